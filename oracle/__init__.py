@@ -1,0 +1,159 @@
+"""CPU oracle for one Fork-dLLM denoising step (binary64, plain C).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+CPU-baseline leg of the benchmark may import this package.  The product path
+(the HIP library and its Python binding) never imports, links or calls it,
+and the two share no code: this package holds its own C source and header and
+reads nothing from the HIP sources.
+
+Functions follow the paper (Fork-dLLM, Section 2 "Sampling in masked dLLMs",
+Algorithm 2, Algorithm 1 for the differential tests, Section 3.2):
+
+* ``row_stats`` -- per-position statistics of q^k(. | x_t): greedy candidate
+  (lowest index of the maximum logit), confidence q(candidate), log q of the
+  candidate, log-normaliser, entropy in nats and the top-2 logit gap.
+* ``select`` -- the unmasking rule inside the active block (threshold set,
+  then leftmost or highest-confidence fallback), applied to copies.
+* ``step`` -- both, over every row.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "fork_oracle.c")
+_LIB = os.path.join(_HERE, "libforkoracle.so")
+
+BF16 = 0
+F32 = 1
+RULE_LEFTMOST = 0
+RULE_MAXCONF = 1
+
+def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the oracle with gcc (plain C99 + OpenMP)."""
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-std=c99", "-O2", "-fopenmp", "-fPIC", "-shared",
+               "-Wall", "-Wextra", "-I", _HERE, "-o", tmp, src, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, out)
+    return out
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _as_input(x: np.ndarray):
+    """bf16 bits arrive as uint16/int16 arrays, binary32 as float32."""
+    x = np.ascontiguousarray(x)
+    if x.dtype in (np.uint16, np.int16):
+        return x, BF16
+    if x.dtype == np.float32:
+        return x, F32
+    raise TypeError("oracle inputs must be bf16 bits (uint16) or float32, got %s" % x.dtype)
+
+
+class Oracle:
+    """ctypes front end of one compiled copy of the oracle."""
+
+    def __init__(self, libpath: str = _LIB):
+        if libpath == _LIB and not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(libpath)
+        P = ctypes.c_void_p
+        lib.oracle_row_stats.restype = ctypes.c_int
+        lib.oracle_row_stats.argtypes = [P, P, ctypes.c_int, ctypes.c_int64,
+                                         ctypes.c_int64, P, ctypes.c_int64,
+                                         P, P, P, P, P, P, ctypes.c_int]
+        lib.oracle_select.restype = ctypes.c_int
+        lib.oracle_select.argtypes = [ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int32, P, P, ctypes.c_double,
+                                      ctypes.c_int, P, P, P, P, P]
+        self.lib = lib
+
+    def row_stats(self, hidden, W, rows=None, nthreads: int = 0):
+        """Statistics of q(. | x_t) for ``rows`` of ``hidden`` ([M, d])
+        against ``W`` ([V, d]); a dict of arrays indexed like ``rows``."""
+        h, dt_h = _as_input(hidden)
+        w, dt_w = _as_input(W)
+        if dt_h != dt_w:
+            raise TypeError("hidden and W must share a dtype")
+        M, d = h.shape
+        V, d2 = w.shape
+        if d != d2:
+            raise ValueError("hidden is [M, %d] but W is [V, %d]" % (d, d2))
+        if rows is None:
+            rows = np.arange(M, dtype=np.int64)
+        rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64)).reshape(-1)
+        if rows.size and (rows.min() < 0 or rows.max() >= M):
+            raise IndexError("row index out of range")
+        n = rows.size
+        out = {k: np.empty(n, np.float64) for k in ("conf", "entropy", "logp", "lse", "gap")}
+        out["argmax"] = np.empty(n, np.int32)
+        rc = self.lib.oracle_row_stats(_ptr(h), _ptr(w), dt_h, d, V, _ptr(rows), n,
+                                       _ptr(out["conf"]), _ptr(out["entropy"]),
+                                       _ptr(out["logp"]), _ptr(out["lse"]),
+                                       _ptr(out["argmax"]), _ptr(out["gap"]),
+                                       int(nthreads))
+        if rc == -2:
+            raise FloatingPointError("non-finite logit")
+        if rc != 0:
+            raise ValueError("oracle_row_stats rejected its arguments (%d)" % rc)
+        return out
+
+    def select(self, conf, argmax_tok, tokens, mask, block_start, B, L,
+               block_len, lam, rule=RULE_LEFTMOST):
+        """Apply the unmasking rule; returns new (tokens, mask, block_start,
+        fallback, ncommit) and leaves the inputs untouched."""
+        conf = np.ascontiguousarray(conf, dtype=np.float64).reshape(-1)
+        argmax_tok = np.ascontiguousarray(argmax_tok, dtype=np.int32).reshape(-1)
+        tok = np.array(tokens, dtype=np.int32, copy=True).reshape(-1)
+        msk = np.array(mask, dtype=np.uint8, copy=True).reshape(-1)
+        bs = np.array(block_start, dtype=np.int32, copy=True).reshape(-1)
+        if conf.size != B * L or argmax_tok.size != B * L or tok.size != B * L \
+                or msk.size != B * L or bs.size != B:
+            raise ValueError("array sizes do not match B=%d, L=%d" % (B, L))
+        fb = np.empty(B, np.int32)
+        nc = np.empty(B, np.int32)
+        rc = self.lib.oracle_select(B, L, block_len, _ptr(conf), _ptr(argmax_tok),
+                                    float(lam), int(rule), _ptr(tok), _ptr(msk),
+                                    _ptr(bs), _ptr(fb), _ptr(nc))
+        if rc != 0:
+            raise ValueError("oracle_select rejected its arguments (%d)" % rc)
+        return tok, msk, bs, fb, nc
+
+    def step(self, hidden, W, tokens, mask, block_start, B, L, block_len, lam,
+             rule=RULE_LEFTMOST, nthreads: int = 0):
+        """One full step on every row: statistics, then selection."""
+        st = self.row_stats(hidden, W, None, nthreads)
+        tok, msk, bs, fb, nc = self.select(st["conf"], st["argmax"], tokens, mask,
+                                           block_start, B, L, block_len, lam, rule)
+        st.update(tokens=tok, mask=msk, block_start=bs, fallback=fb, ncommit=nc)
+        return st
+
+
+_default = None
+
+
+def default() -> Oracle:
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default
+
+
+def row_stats(*a, **k):
+    return default().row_stats(*a, **k)
+
+
+def select(*a, **k):
+    return default().select(*a, **k)
+
+
+def step(*a, **k):
+    return default().step(*a, **k)

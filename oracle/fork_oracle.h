@@ -1,0 +1,80 @@
+/*
+ * fork_oracle.h -- CPU reference (oracle) for one Fork-dLLM denoising step.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing on the product path links, loads or calls
+ * this code; only the test suite, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code, header, table or constant with the HIP
+ * library, and it does not include any HIP header.
+ *
+ * Everything is computed in IEEE binary64 from the same input bits the GPU
+ * path reads (bf16 or binary32 values are widened exactly).  No blocking,
+ * fusion or re-ordering is applied beyond what the definitions state.
+ *
+ * Paper: "Fork-dLLM: Avoiding the Flexibility Trap in Diffusion Language
+ * Models", Section 2 (Sampling in masked dLLMs), Algorithm 2 (Fork-dLLM),
+ * Algorithm 1 (Fast-dLLM, for the differential tests), Section 3.2 (fallback
+ * step set F_i and the ratio at k_{i,t}).
+ */
+#ifndef FORK_ORACLE_H
+#define FORK_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORACLE_BF16 = 0, ORACLE_F32 = 1 };
+enum { ORACLE_RULE_LEFTMOST = 0,   /* Fork-dLLM fallback (Algorithm 2)  */
+       ORACLE_RULE_MAXCONF = 1 };  /* Fast-dLLM fallback (Algorithm 1)  */
+
+/*
+ * Per-position statistics of the model distribution q^k(. | x_t) for the
+ * rows listed in `rows` (indices into the [M, d] hidden matrix).
+ *
+ *   z_v      = sum_j h_j * W[v, j]               (j ascending, binary64)
+ *   argmax   = lowest v with z_v = max_u z_u      (greedy candidate x_0^k)
+ *   lse      = log sum_v exp(z_v)
+ *   conf     = q(argmax) = exp(z_argmax - lse)   (confidence c_t^k)
+ *   logp     = log q(argmax) = z_argmax - lse    (numerator/denominator of rho)
+ *   entropy  = -sum_v q_v log q_v                 (nats)
+ *   gap      = z_argmax - max_{v != argmax} z_v  (0 if V == 1; tie diagnostics)
+ *
+ * Any output pointer may be NULL.  Outputs are indexed by position in `rows`.
+ * nthreads <= 0 means "use OpenMP's default".  Returns 0, or -1 on bad
+ * arguments, -2 if a logit is not finite.
+ */
+int oracle_row_stats(const void* hidden, const void* W, int dtype,
+                     int64_t d, int64_t V,
+                     const int64_t* rows, int64_t nrows,
+                     double* conf, double* entropy, double* logp, double* lse,
+                     int32_t* argmax, double* gap, int nthreads);
+
+/*
+ * One application of the unmasking rule to B sequences of length L, in place.
+ *
+ * Active block of sequence b: the first block [s, min(s+BL, L)) with
+ * s = block_start[b] + j*BL (j = 0, 1, ...) that holds a masked position.
+ * Inside it, with M the masked positions:
+ *   U = { k in M : conf[k] > lambda }                       (strict)
+ *   if U is empty:  U = { leftmost(M) }       (rule LEFTMOST, Algorithm 2)
+ *                   U = { argmax_k conf[k] }  (rule MAXCONF,  Algorithm 1;
+ *                                              ties -> lowest k)
+ *   tokens[k] = argmax_tok[k], mask[k] = 0 for k in U.
+ * fallback[b] = 1 if U was empty before the fallback, 0 otherwise, and -1
+ * (nothing written, block_start unchanged) when no masked position exists at
+ * or after block_start[b].  block_start[b] is set to the active block's start.
+ * ncommit[b] (may be NULL) receives |U|.
+ * Arrays conf / argmax_tok / tokens / mask are [B*L], row b*L + position.
+ * Returns 0, or -1 on bad arguments.
+ */
+int oracle_select(int32_t B, int32_t L, int32_t block_len,
+                  const double* conf, const int32_t* argmax_tok,
+                  double lambda, int rule,
+                  int32_t* tokens, uint8_t* mask, int32_t* block_start,
+                  int32_t* fallback, int32_t* ncommit);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,85 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case copies the oracle's C source to a temporary directory, plants one
+mistake (a dropped term, a wrong sign or index, a transposed operand, a
+non-strict threshold, ...), compiles the copy and runs the pin checks of
+test_oracle_pins against it: at least one must fail.  Nothing here touches
+the real oracle or any GPU.
+"""
+import os
+import shutil
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "fork_oracle.c")
+HDR = os.path.join(os.path.dirname(oracle.__file__), "fork_oracle.h")
+
+MUTATIONS = {
+    "argmax_tie_highest": ("if (z[v] > z[a]) a = v;", "if (z[v] >= z[a]) a = v;"),
+    "drop_first_product": ("for (int64_t j = 0; j < d; ++j)", "for (int64_t j = 1; j < d; ++j)"),
+    "transposed_weight": ("widen(W, dtype, v * d + j)", "widen(W, dtype, j * V + v)"),
+    "no_max_shift": ("sum += exp(z[v] - zmax);", "sum += exp(z[v]);"),
+    "entropy_sign": ("h -= exp(lq) * lq;", "h += exp(lq) * lq;"),
+    "entropy_drops_norm": ("double lq = z[v] - log_norm;", "double lq = z[v] - zmax;"),
+    "logp_drops_logit": ("*logp = z[a] - log_norm;", "*logp = -log_norm;"),
+    "conf_unnormalised": ("*conf = exp(z[a] - log_norm);", "*conf = exp(z[a] - zmax);"),
+    "threshold_not_strict": ("conf[base + k] > lambda", "conf[base + k] >= lambda"),
+    "no_block_limit": ("const int32_t e = s + block_len < L ? s + block_len : L;",
+                       "const int32_t e = L;"),
+    "rightmost_fallback": ("if (rule == ORACLE_RULE_LEFTMOST) break;",
+                           "if (rule == ORACLE_RULE_LEFTMOST) continue;"),
+    "fallback_flag_swapped": ("fallback[b] = 1;\n    } else {\n      fallback[b] = 0;",
+                              "fallback[b] = 0;\n    } else {\n      fallback[b] = 1;"),
+    "fast_tie_highest": ("} else if (conf[base + k] > conf[base + pick]) {",
+                         "} else if (conf[base + k] >= conf[base + pick]) {"),
+    "no_skip_forward": ("s += block_len;", "break;"),
+}
+
+
+def _checks(orc):
+    """Run the pin suite's checks against one oracle build; returns the
+    number of failing checks."""
+    calls = [
+        lambda: pins.test_stats_match_dense_brute_force(orc, 1, 7, 16, 33, "f32", 1.0),
+        lambda: pins.test_stats_match_dense_brute_force(orc, 3, 9, 40, 257, "bf16", 3.0),
+        lambda: pins.test_uniform_closed_form(orc, 1024),
+        lambda: pins.test_k_way_tie_closed_form(orc, 7, 0),
+        lambda: pins.test_two_level_closed_form(orc, 3.0, 0.0, 10),
+        lambda: pins.test_shift_invariance(orc),
+        lambda: pins.test_select_hand_worked_fixture(orc),
+        lambda: pins.test_lambda_at_least_one_is_autoregressive(orc, 1.0),
+        lambda: pins.test_lambda_zero_commits_whole_blocks(orc),
+        lambda: pins.test_select_invariants(orc, 0, 0.8),
+        lambda: pins.test_fork_vs_fast_differential(orc, 0),
+        lambda: pins.test_fast_fallback_tie_takes_lowest_position(orc),
+    ]
+    failed = 0
+    for c in calls:
+        try:
+            c()
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            failed += 1
+    return failed
+
+
+def test_unmutated_copy_passes(tmp_path):
+    shutil.copy(HDR, tmp_path)
+    src = tmp_path / "fork_oracle.c"
+    shutil.copy(SRC, src)
+    lib = oracle.build(force=True, src=str(src), out=str(tmp_path / "lib.so"))
+    assert _checks(oracle.Oracle(lib)) == 0
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    old, new = MUTATIONS[name]
+    text = open(SRC).read()
+    assert text.count(old) == 1, "mutation anchor must occur exactly once"
+    shutil.copy(HDR, tmp_path)
+    src = tmp_path / "fork_oracle.c"
+    src.write_text(text.replace(old, new))
+    lib = oracle.build(force=True, src=str(src), out=str(tmp_path / ("%s.so" % name)))
+    assert _checks(oracle.Oracle(lib)) > 0, "planted mistake %r went unnoticed" % name

@@ -1,0 +1,342 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these tests re-types the oracle's formulas: statistics are checked
+against scipy's log-sum-exp / entropy on logits from numpy's matmul, against
+closed forms, and against invariants; the selection rule against a
+hand-worked fixture (tests/golden/select_worked.json), the special cases
+lambda >= 1 (autoregressive order) and lambda = 0 (whole blocks), and the
+Fork-vs-Fast differential (Algorithm 1 vs Algorithm 2).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+import torch
+
+import oracle
+from paper_2609_39859_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bf16_bits(x: np.ndarray) -> np.ndarray:
+    return synth.to_bits(torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16))
+
+
+def _bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    if bits.dtype == np.uint16:
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    return bits.astype(np.float64)
+
+
+def _brute(hbits, wbits):
+    """Dense reference: numpy fp64 matmul, scipy log-softmax and entropy."""
+    z = _bits_to_f64(hbits) @ _bits_to_f64(wbits).T
+    lsm = scipy.special.log_softmax(z, axis=1)
+    p = np.exp(lsm)
+    ent = scipy.stats.entropy(p, axis=1)
+    am = np.argmax(z, axis=1)              # numpy: first (lowest) index
+    lse = scipy.special.logsumexp(z, axis=1)
+    return z, p, ent, am, lse
+
+
+@pytest.mark.parametrize("seed,M,d,V,dtype,scale", [
+    (1, 7, 16, 33, "f32", 1.0),
+    (2, 5, 64, 1024, "f32", 8.0),
+    (3, 9, 40, 257, "bf16", 3.0),
+    (4, 4, 256, 1000, "bf16", 0.05),
+    (5, 3, 8, 1, "f32", 1.0),
+])
+def test_stats_match_dense_brute_force(orc, seed, M, d, V, dtype, scale):
+    rng = np.random.default_rng(seed)
+    h = (rng.standard_normal((M, d)) * scale).astype(np.float32)
+    w = (rng.standard_normal((V, d)) / math.sqrt(d)).astype(np.float32)
+    if dtype == "bf16":
+        h, w = _bf16_bits(h), _bf16_bits(w)
+    st = orc.row_stats(h, w)
+    z, p, ent, am, lse = _brute(h, w)
+    assert np.array_equal(st["argmax"], am)
+    np.testing.assert_allclose(st["lse"], lse, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(st["conf"], p[np.arange(M), am], rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(st["logp"], np.log(p[np.arange(M), am]), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(st["entropy"], ent, rtol=1e-10, atol=1e-12)
+    zs = np.sort(z, axis=1)
+    gap = zs[:, -1] - zs[:, -2] if V > 1 else np.zeros(M)
+    np.testing.assert_allclose(st["gap"], gap, rtol=1e-12, atol=1e-12)
+
+
+def test_row_subset_and_order(orc):
+    rng = np.random.default_rng(7)
+    h = rng.standard_normal((12, 32)).astype(np.float32)
+    w = rng.standard_normal((50, 32)).astype(np.float32)
+    full = orc.row_stats(h, w)
+    rows = np.array([11, 0, 5, 5, 3])
+    sub = orc.row_stats(h, w, rows)
+    for k in ("conf", "entropy", "logp", "lse", "argmax", "gap"):
+        assert np.array_equal(sub[k], full[k][rows])
+
+
+@pytest.mark.parametrize("V", [1, 2, 1024, 126464 // 64])
+def test_uniform_closed_form(orc, V):
+    """W = 0: every logit is 0, q is uniform: conf = 1/V, H = log V,
+    log q = -log V, candidate = index 0 (lowest of a V-way tie)."""
+    h = np.ones((3, 8), np.float32)
+    w = np.zeros((V, 8), np.float32)
+    st = orc.row_stats(h, w)
+    assert np.all(st["argmax"] == 0)
+    np.testing.assert_allclose(st["conf"], 1.0 / V, rtol=1e-13)
+    np.testing.assert_allclose(st["entropy"], math.log(V), rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(st["logp"], -math.log(V), rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(st["lse"], math.log(V), rtol=1e-13, atol=1e-15)
+    assert np.all(st["gap"] == 0.0)
+
+
+@pytest.mark.parametrize("k,first", [(1, 5), (2, 3), (7, 0), (16, 60)])
+def test_k_way_tie_closed_form(orc, k, first):
+    """k tied logits at 5, the rest at -1000: conf = 1/k, H = log k,
+    candidate = the lowest tied index."""
+    V = 128
+    tied = [first + 3 * i for i in range(k)]
+    w = np.full((V, 1), -1000.0, np.float32)
+    w[tied, 0] = 5.0
+    h = np.ones((1, 1), np.float32)
+    st = orc.row_stats(h, w)
+    assert st["argmax"][0] == tied[0]
+    np.testing.assert_allclose(st["conf"][0], 1.0 / k, rtol=1e-13)
+    np.testing.assert_allclose(st["entropy"][0], math.log(k), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(st["logp"][0], -math.log(k), rtol=1e-13, atol=1e-15)
+    assert st["gap"][0] == (0.0 if k > 1 else 1005.0)
+
+
+@pytest.mark.parametrize("a,b,V", [(3.0, 0.0, 10), (0.0, 2.0, 5), (100.0, 0.0, 1000), (-7.5, -8.0, 300)])
+def test_two_level_closed_form(orc, a, b, V):
+    """One logit a at index 1, the other V-1 at b:
+    q1 = 1 / (1 + (V-1) e^(b-a)), q2 = e^(b-a) q1,
+    H = -q1 log q1 - (V-1) q2 log q2."""
+    w = np.full((V, 1), b, np.float32)
+    w[1, 0] = a
+    st = orc.row_stats(np.ones((1, 1), np.float32), w)
+    r = math.exp(b - a)
+    q1 = 1.0 / (1.0 + (V - 1) * r)
+    q2 = r * q1
+    H = -q1 * math.log(q1) - (V - 1) * (q2 * math.log(q2) if q2 > 0 else 0.0)
+    top = 1 if a > b else 0
+    assert st["argmax"][0] == top
+    conf = q1 if a > b else q2
+    np.testing.assert_allclose(st["conf"][0], conf, rtol=1e-12)
+    np.testing.assert_allclose(st["entropy"][0], H, rtol=1e-10, atol=1e-30)
+    np.testing.assert_allclose(st["logp"][0], math.log(conf), rtol=1e-12, atol=1e-14)
+
+
+def test_shift_invariance(orc):
+    """q is unchanged when every logit moves by the same constant c (an extra
+    input column with h = 1 and W = c): only the log-normaliser moves."""
+    rng = np.random.default_rng(11)
+    h = rng.standard_normal((6, 24)).astype(np.float32)
+    w = (rng.standard_normal((200, 24)) / 5).astype(np.float32)
+    base = orc.row_stats(h, w)
+    c = 37.25
+    h2 = np.concatenate([h, np.ones((6, 1), np.float32)], axis=1)
+    w2 = np.concatenate([w, np.full((200, 1), c, np.float32)], axis=1)
+    sh = orc.row_stats(h2, w2)
+    assert np.array_equal(sh["argmax"], base["argmax"])
+    np.testing.assert_allclose(sh["conf"], base["conf"], rtol=1e-11)
+    np.testing.assert_allclose(sh["entropy"], base["entropy"], rtol=1e-11)
+    np.testing.assert_allclose(sh["lse"], base["lse"] + c, rtol=1e-12)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_peaked"])
+def test_stat_invariants_on_workload(orc, name):
+    cfg = synth.CONFIGS[name]
+    W = synth.to_bits(synth.weights(cfg))
+    h = synth.to_bits(synth.hidden(cfg, 0))
+    st = orc.row_stats(h, W)
+    V = cfg.V
+    assert np.all(st["entropy"] >= -1e-12)
+    assert np.all(st["entropy"] <= math.log(V) + 1e-12)
+    assert np.all(st["conf"] >= 1.0 / V - 1e-15) and np.all(st["conf"] <= 1.0)
+    np.testing.assert_allclose(st["logp"], np.log(st["conf"]), rtol=1e-12, atol=1e-12)
+    assert np.all(st["gap"] >= 0.0)
+    # a confident row has low entropy: H <= -log conf * ... (H >= 0 and
+    # H <= log V always; for conf > 1/2, H <= h2(conf) + (1-conf) log(V-1))
+    hi = st["conf"] > 0.5
+    c = st["conf"][hi]
+    bound = -c * np.log(c) - (1 - c) * np.log1p(-c) + (1 - c) * math.log(V - 1)
+    assert np.all(st["entropy"][hi] <= bound + 1e-12)
+
+
+def test_non_finite_input_is_refused(orc):
+    h = np.ones((1, 2), np.float32)
+    w = np.array([[np.inf, 0.0]], np.float32)
+    with pytest.raises(FloatingPointError):
+        orc.row_stats(h, w)
+
+
+# ---------------------------------------------------------------- selection
+
+def _golden():
+    with open(os.path.join(GOLDEN, "select_worked.json")) as f:
+        return json.load(f)
+
+
+def test_select_hand_worked_fixture(orc):
+    g = _golden()
+    B, L, BL, lam = g["B"], g["L"], g["block_len"], g["lambda"]
+    tok = np.array(g["initial"]["tokens"], np.int32)
+    msk = np.array(g["initial"]["mask"], np.uint8)
+    bs = np.array(g["initial"]["block_start"], np.int32)
+    for st in g["steps"]:
+        conf = np.array(st["conf"])
+        am = np.array(st["argmax"], np.int32)
+        if "fast" in st:
+            ft, fm, fb_, ff, fn = orc.select(conf, am, tok, msk, bs, B, L, BL, lam,
+                                             rule=oracle.RULE_MAXCONF)
+            exp = st["fast"]
+            assert ft.tolist() == exp["tokens"] and fm.tolist() == exp["mask"]
+            assert fb_.tolist() == exp["block_start"] and ff.tolist() == exp["fallback"]
+            assert fn.tolist() == exp["ncommit"]
+        tok, msk, bs, fb, nc = orc.select(conf, am, tok, msk, bs, B, L, BL, lam)
+        exp = st["fork"]
+        assert tok.tolist() == exp["tokens"]
+        assert msk.tolist() == exp["mask"]
+        assert bs.tolist() == exp["block_start"]
+        assert fb.tolist() == exp["fallback"]
+        assert nc.tolist() == exp["ncommit"]
+
+
+def _decode_random_conf(orc, B, P, G, BL, lam, seed, rule=oracle.RULE_LEFTMOST, steps_cap=None):
+    """Decode with i.i.d. random confidences each step; returns the per-step
+    history of committed positions and flags."""
+    rng = np.random.default_rng(seed)
+    L = P + G
+    tok = np.full(B * L, -1, np.int32)
+    msk = np.zeros(B * L, np.uint8)
+    for b in range(B):
+        msk[b * L + P: (b + 1) * L] = 1
+    bs = np.full(B, P, np.int32)
+    hist = []
+    for t in range(steps_cap or (G + 2)):
+        if not msk.any():
+            break
+        conf = rng.random(B * L)
+        am = rng.integers(0, 1000, B * L).astype(np.int32)
+        prev = msk.copy()
+        tok, msk, bs, fb, nc = orc.select(conf, am, tok, msk, bs, B, L, BL, lam, rule)
+        newly = np.nonzero(prev.astype(bool) & ~msk.astype(bool))[0]
+        assert np.all(msk <= prev), "mask must be monotone"
+        assert np.all(tok[newly] == am[newly]), "committed token is the candidate"
+        hist.append((newly, fb.copy(), nc.copy(), conf, prev))
+    return hist, msk
+
+
+@pytest.mark.parametrize("lam", [1.0, 2.0])
+def test_lambda_at_least_one_is_autoregressive(orc, lam):
+    """conf <= 1 never passes lambda >= 1, so every step is a fallback step
+    and Fork-dLLM commits P, P+1, ... (AR decoding, Section 2): T = G."""
+    B, P, G, BL = 3, 5, 20, 6
+    hist, msk = _decode_random_conf(orc, B, P, G, BL, lam, seed=3)
+    assert len(hist) == G and not msk.any()
+    L = P + G
+    for t, (newly, fb, nc, _, _) in enumerate(hist):
+        assert fb.tolist() == [1] * B and nc.tolist() == [1] * B
+        assert sorted(newly.tolist()) == [b * L + P + t for b in range(B)]
+
+
+def test_lambda_zero_commits_whole_blocks(orc):
+    """conf >= 1/V > 0 passes lambda = 0 everywhere: each step commits the
+    whole active block, T = ceil(G / BL), no fallback."""
+    B, P, G, BL = 2, 3, 21, 8
+    hist, msk = _decode_random_conf(orc, B, P, G, BL, 0.0, seed=4)
+    assert len(hist) == math.ceil(G / BL) and not msk.any()
+    for t, (newly, fb, nc, _, _) in enumerate(hist):
+        assert fb.tolist() == [0] * B
+        assert nc.tolist() == [min(BL, G - t * BL)] * B
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("lam", [0.5, 0.8, 0.95])
+def test_select_invariants(orc, seed, lam):
+    B, P, G, BL = 4, 7, 40, 8
+    L = P + G
+    hist, msk = _decode_random_conf(orc, B, P, G, BL, lam, seed=seed)
+    assert not msk.any() and len(hist) <= G
+    for newly, fb, nc, conf, prev in hist:
+        for b in range(B):
+            mine = [k - b * L for k in newly if b * L <= k < (b + 1) * L]
+            masked = [k for k in range(P, L) if prev[b * L + k]]
+            if not masked:
+                assert fb[b] == -1 and not mine
+                continue
+            # active block: the one holding the leftmost masked position
+            s = P + ((masked[0] - P) // BL) * BL
+            blk = [k for k in masked if s <= k < s + BL]
+            best = max(conf[b * L + k] for k in blk)
+            assert all(s <= k < s + BL for k in mine)
+            assert nc[b] == len(mine) >= 1
+            if fb[b] == 1:
+                assert best <= lam and mine == [blk[0]]
+            else:
+                assert fb[b] == 0 and best > lam
+                assert mine == [k for k in blk if conf[b * L + k] > lam]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fork_vs_fast_differential(orc, seed):
+    """Algorithms 1 and 2 differ only in the fallback: the same inputs give
+    the same commit set on parallel steps; on fallback steps Fork takes the
+    leftmost masked position and Fast the highest confidence one."""
+    rng = np.random.default_rng(100 + seed)
+    B, L, BL, lam = 5, 30, 10, 0.7
+    for _ in range(20):
+        msk = (rng.random(B * L) < 0.6).astype(np.uint8)
+        tok = np.where(msk, -1, 3).astype(np.int32)
+        bs = rng.integers(0, 3, B).astype(np.int32) * BL
+        conf = rng.random(B * L) * rng.choice([0.8, 1.0], B * L)
+        am = rng.integers(0, 99, B * L).astype(np.int32)
+        fk = orc.select(conf, am, tok, msk, bs, B, L, BL, lam, oracle.RULE_LEFTMOST)
+        fs = orc.select(conf, am, tok, msk, bs, B, L, BL, lam, oracle.RULE_MAXCONF)
+        assert np.array_equal(fk[2], fs[2]) and np.array_equal(fk[3], fs[3])
+        for b in range(B):
+            sl = slice(b * L, (b + 1) * L)
+            if fk[3][b] != 1:
+                assert np.array_equal(fk[1][sl], fs[1][sl])
+                continue
+            s = fk[2][b]
+            blk = [k for k in range(s, min(s + BL, L)) if msk[b * L + k]]
+            fork_pick = [k for k in range(L) if msk[b * L + k] and not fk[1][b * L + k]]
+            fast_pick = [k for k in range(L) if msk[b * L + k] and not fs[1][b * L + k]]
+            assert fork_pick == [blk[0]]
+            c = [conf[b * L + k] for k in blk]
+            assert fast_pick == [blk[int(np.argmax(c))]]
+
+
+def test_select_rejects_bad_arguments(orc):
+    z = np.zeros(8)
+    a = np.zeros(8, np.int32)
+    t = np.zeros(8, np.int32)
+    m = np.ones(8, np.uint8)
+    with pytest.raises(ValueError):
+        orc.select(z, a, t, m, np.array([0], np.int32), 1, 8, 0, 0.5)
+    with pytest.raises(ValueError):
+        orc.select(z, a, t, m, np.array([9], np.int32), 1, 8, 4, 0.5)
+    with pytest.raises(ValueError):
+        orc.select(z, a, t, m, np.array([0], np.int32), 1, 8, 4, 0.5, rule=7)
+
+
+def test_fast_fallback_tie_takes_lowest_position(orc):
+    """Algorithm 1's argmax over positions is silent on ties; the reading
+    taken is the lowest position.  Masked {1, 2, 3}, conf (0.3, 0.4, 0.4),
+    lambda = 0.5: Fast commits 2, Fork commits 1."""
+    conf = np.array([0.0, 0.3, 0.4, 0.4])
+    am = np.array([0, 5, 6, 7], np.int32)
+    tok = np.array([9, -1, -1, -1], np.int32)
+    msk = np.array([0, 1, 1, 1], np.uint8)
+    bs = np.array([1], np.int32)
+    t, m, _, fb, _ = orc.select(conf, am, tok, msk, bs, 1, 4, 3, 0.5, oracle.RULE_MAXCONF)
+    assert t.tolist() == [9, -1, 6, -1] and m.tolist() == [0, 1, 0, 1] and fb.tolist() == [1]
+    t, m, _, fb, _ = orc.select(conf, am, tok, msk, bs, 1, 4, 3, 0.5, oracle.RULE_LEFTMOST)
+    assert t.tolist() == [9, 5, -1, -1] and m.tolist() == [0, 0, 1, 1] and fb.tolist() == [1]
