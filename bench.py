@@ -1,0 +1,216 @@
+"""Benchmark of the Fork-dLLM denoising step on one MI355X.
+
+A step is one fork_step call (LM-head GEMM with the fused per-tile
+statistics, the cross-tile merge, and the per-sequence selection) over one
+batch of synthetic hidden states already resident in HBM.  The workload is
+the LLaDA-8B-shaped configuration: B=8 sequences of L=512 positions
+(256 prompt + 256 generation), block length 32, d=4096, V=126464, bf16
+inputs with fp32 accumulation, threshold 0.9.
+
+Prints ONE JSON line.  `value` is denoising steps per second; positions per
+second (B*L rows through the LM head) is reported beside it.  `roofline`
+covers the dominant kernel (the LM-head GEMM + statistics), timed with HIP
+events recorded around that kernel alone on the stream it runs on.
+`cpu_baseline` times the binary64 CPU oracle on a bounded sample of rows of
+the same workload and scales it to steps per second.
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "denoising steps/sec and positions/sec at B·L×4096×126464; % MFMA bf16 peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_lmhead_llada8b.json")
+LMHEAD_SRC = os.path.join(ROOT, "paper_2609_39859_amd", "csrc", "gemm_stats.hip")
+
+
+def _hip():
+    """The HIP runtime torch already loaded (same soname)."""
+    lib = ctypes.CDLL("libamdhip64.so.7")
+    lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    lib.hipEventCreate.restype = ctypes.c_int
+    lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    lib.hipEventDestroy.restype = ctypes.c_int
+    lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    lib.hipEventElapsedTime.restype = ctypes.c_int
+    return lib
+
+
+def _source_hash():
+    with open(LMHEAD_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _traffic_per_launch():
+    """HBM bytes per LM-head launch from the committed rocprofv3 counter runs,
+    if they were taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != _source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(cfg, W_dev, h_dev, target_s):
+    """Time the oracle (as it is) on a bounded sample of rows of this
+    workload; scale rows/s to steps/s (a step covers B*L rows)."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_39859_amd import synth
+    Wb = synth.to_bits(W_dev)
+    hb = synth.to_bits(h_dev)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count() or 1
+    orc = oracle.default()
+    probe = np.arange(threads, dtype=np.int64)
+    t0 = time.perf_counter()
+    orc.row_stats(hb, Wb, probe, nthreads=threads)
+    per_batch = time.perf_counter() - t0
+    nb = max(1, int(target_s / max(per_batch, 1e-3)) - 1)
+    rows = np.arange(threads, threads * (nb + 1), dtype=np.int64) % cfg.M
+    t0 = time.perf_counter()
+    st = orc.row_stats(hb, Wb, rows, nthreads=threads)
+    dt = time.perf_counter() - t0
+    assert np.all(np.isfinite(st["conf"]))
+    rows_per_s = rows.size / dt
+    return {"value": rows_per_s / cfg.M, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of the %d rows of one step (binary64 logits over all %d vocabulary "
+                      "entries + statistics), %.1f s on %d threads; value = rows/s / %d"
+                      % (rows.size, cfg.M, cfg.V, dt, threads, cfg.M)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="llada8b")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_39859_amd import _binding, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.config]
+    B, L, BL, M, d, V = cfg.B, cfg.L, cfg.block_len, cfg.M, cfg.d, cfg.V
+    print("bench: %s B=%d L=%d d=%d V=%d, generating inputs" % (cfg.name, B, L, d, V),
+          file=sys.stderr, flush=True)
+
+    W = synth.weights(cfg, device=dev)
+    n_batches = 4
+    hs = [synth.hidden(cfg, t, device=dev) for t in range(n_batches)]
+    tok0, msk0, bs0 = synth.initial_state(cfg)
+    tok, msk, bs = tok0.to(dev), msk0.to(dev), bs0.to(dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
+    fb = torch.empty(B, dtype=torch.int32, device=dev)
+
+    hip = _hip()
+    n_ev = args.steps
+    evs = []
+    for _ in range(2 * n_ev):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+        evs.append(e.value)
+
+    def step(i, events=None):
+        _binding.fork_step_ex(hs[i % n_batches], W, tok, msk, bs, BL, cfg.tau, conf, ent, logp,
+                              fb, B=B, L=L, events=events)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    # restart the decode so every timed step has masked positions to select
+    tok.copy_(tok0.to(dev))
+    msk.copy_(msk0.to(dev))
+    bs.copy_(bs0.to(dev))
+    torch.cuda.synchronize()
+    print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
+
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        step(i, (evs[2 * i], evs[2 * i + 1]))
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start.elapsed_time(stop)
+    lm_ms = []
+    for i in range(n_ev):
+        ms = ctypes.c_float()
+        assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
+        lm_ms.append(ms.value)
+    for e in evs:
+        hip.hipEventDestroy(e)
+
+    ms_per_step = total_ms / args.steps
+    steps_per_s = 1000.0 / ms_per_step
+    lm_avg_ms = sum(lm_ms) / len(lm_ms)
+    flops = 2.0 * M * d * V
+    achieved_tflops = flops / (lm_avg_ms * 1e-3) / 1e12
+    traffic = _traffic_per_launch()
+
+    out = {
+        "metric": METRIC,
+        "value": steps_per_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) hidden rows x RMS~U[0.5,2], W_head ~ N(0,1/d); no model weights)",
+        "config": {"workload": "LLaDA-8B-shaped step: B=8, L=512 (prompt 256 + gen 256), block_len 32, "
+                               "d=4096, V=126464, bf16, tau=0.9",
+                   "B": B, "L": L, "block_len": BL, "d": d, "V": V, "tau": cfg.tau},
+        "positions_per_s": steps_per_s * M,
+        "mfma_frac_step": (flops / (ms_per_step * 1e-3) / 1e12) / PEAK_BF16_TFLOPS,
+        "lmhead_ms": lm_avg_ms,
+        "wall_s_timed": wall,
+        "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": traffic,
+                     "kernel": "gemm_stats_kernel<bf16> (LM head + per-tile statistics)",
+                     "algorithmic_flops_per_launch": flops},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

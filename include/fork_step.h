@@ -1,0 +1,169 @@
+/*
+ * fork_step.h -- C ABI of the MI355X (gfx950) Fork-dLLM denoising step.
+ *
+ * One call performs one denoising step of the Fork-dLLM sampler (Fork-dLLM
+ * paper, Section 2 "Sampling in masked dLLMs" and Algorithm 2) for B
+ * sequences of L positions:
+ *
+ *   1. logits z[r, v] = sum_j hidden[r, j] * W_head[v, j] for every position
+ *      r < B*L and vocabulary entry v < V (the LM-head projection that yields
+ *      the model's per-position categorical q^k(. | x_t));
+ *   2. per position: greedy candidate x_0 = argmax_v z (lowest v on ties),
+ *      confidence c = q(x_0) (Section 2), log q(x_0) (the quantity inside the
+ *      ForkGRPO ratio, Section 3.2), entropy -sum q log q in nats (Section
+ *      3.1) and, optionally, the log-normaliser;
+ *   3. per sequence, inside its active block of the semi-autoregressive
+ *      regime (Section 4.1): commit every masked position with c > tau
+ *      (strict); if there is none, commit only the leftmost masked position
+ *      (Algorithm 2) and report a fallback step (membership of the step in
+ *      the set F_i of Section 3.2).
+ *
+ * `tau` is the paper's confidence threshold lambda.  Candidates are greedy
+ * (sampling temperature 0).  The [B*L, V] logits are never written to memory.
+ *
+ * Conventions shared by every entry point
+ *   - All array arguments are DEVICE pointers (HIP device memory of the
+ *     current device) owned by the caller; the library never frees them.
+ *   - Row-major layouts; position r of sequence b is row b*L + r.
+ *   - The call is asynchronous: work is enqueued on `stream` (a hipStream_t,
+ *     NULL = the legacy default stream) and the function returns without
+ *     synchronising (unless the environment sets FORK_SYNC=1, a debugging aid
+ *     that synchronises and reports launch-time errors).
+ *   - Argument errors are detected on the host before anything is enqueued
+ *     and return a negative status; fork_last_error() then describes them.
+ *   - Output arrays must not alias inputs.  tokens, mask and block_start are
+ *     updated in place.
+ *   - Concurrent calls that use the library-managed workspace must be issued
+ *     on one stream (or serialised by the caller); callers that overlap
+ *     calls on several streams pass their own workspace to fork_step_ex.
+ */
+#ifndef FORK_STEP_H
+#define FORK_STEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+enum {
+  FORK_OK = 0,
+  FORK_EINVAL = -1,       /* bad argument (null pointer, size, alignment, tau)  */
+  FORK_EUNSUPPORTED = -2, /* valid but unsupported (d not a multiple of 8 / 4) */
+  FORK_EHIP = -3,         /* a HIP runtime call or launch failed               */
+  FORK_ENOMEM = -4        /* the library-managed workspace could not grow      */
+};
+
+/* Element types of hidden and W_head (both the same). */
+enum { FORK_BF16 = 0, FORK_F32 = 1 };
+
+/* Fallback rules when no masked position of the active block passes tau. */
+enum {
+  FORK_RULE_LEFTMOST = 0, /* Fork-dLLM, Algorithm 2: the leftmost masked position */
+  FORK_RULE_MAXCONF = 1   /* Fast-dLLM, Algorithm 1: the highest confidence
+                             (lowest position on ties)                          */
+};
+
+/* Values written to out_fallback[b]. */
+enum {
+  FORK_STEP_PARALLEL = 0, /* at least one position passed tau, all committed   */
+  FORK_STEP_FALLBACK = 1, /* none passed; exactly one position committed       */
+  FORK_STEP_IDLE = -1,    /* no masked position at or after block_start[b]     */
+  FORK_STEP_BADSTATE = -2 /* block_start[b] outside [0, L]; nothing written    */
+};
+
+/*
+ * fork_step -- one denoising step (Algorithm 2 with greedy candidates).
+ *
+ * hidden       [B*L, d]  FORK_BF16 or FORK_F32, row-major, 16-byte aligned.
+ *                        Final hidden state of every position.
+ * W_head       [V, d]    same element type, row-major (one row per
+ *                        vocabulary entry), 16-byte aligned.
+ * tokens       [B*L] int32, in/out.  Written only at committed positions,
+ *                        with the candidate token.
+ * mask         [B*L] uint8, in/out.  Nonzero = [MASK].  Cleared at committed
+ *                        positions.  Only positions at or after block_start[b]
+ *                        are considered.
+ * block_start  [B] int32, in/out.  Start of the block to resume from; the
+ *                        active block is the first block [s, min(s+block_len,
+ *                        L)), s = block_start[b] + j*block_len, that holds a
+ *                        masked position; its start is written back.
+ * block_len    1 <= block_len <= L.
+ * tau          the confidence threshold (lambda); finite.  Commit iff
+ *                        conf > tau, compared in binary32.
+ * out_conf     [B*L] float: q(candidate) for every position.
+ * out_entropy  [B*L] float: entropy of q in nats for every position.
+ * out_logp     [B*L] float: log q(candidate) for every position.
+ * out_fallback [B] int32: FORK_STEP_* per sequence.
+ * B, L, d, V   sizes, all >= 1, B*L < 2^31; d % 8 == 0 for FORK_BF16,
+ *              d % 4 == 0 for FORK_F32.
+ * dtype        FORK_BF16 or FORK_F32.
+ * stream       hipStream_t to enqueue on (NULL = default stream).
+ *
+ * Returns FORK_OK or a negative FORK_E* code.  Uses the library-managed
+ * workspace of the current device (grown on demand with hipMalloc, which may
+ * synchronise the device; fork_release frees it).
+ */
+int fork_step(const void* hidden, const void* W_head, int32_t* tokens,
+              uint8_t* mask, int32_t* block_start, int32_t block_len,
+              float tau, float* out_conf, float* out_entropy, float* out_logp,
+              int32_t* out_fallback, int32_t B, int32_t L, int32_t d,
+              int32_t V, int32_t dtype, void* stream);
+
+/* Arguments of fork_step_ex: those of fork_step plus optional extras. */
+typedef struct fork_step_args {
+  const void* hidden;
+  const void* W_head;
+  int32_t* tokens;
+  uint8_t* mask;
+  int32_t* block_start;
+  int32_t block_len;
+  float tau;
+  float* out_conf;
+  float* out_entropy;
+  float* out_logp;
+  int32_t* out_fallback;
+  int32_t B, L, d, V, dtype;
+  void* stream;
+  /* Optional outputs (NULL = not produced). */
+  float* out_lse;          /* [B*L] log sum_v exp z_v (log-normaliser)        */
+  int32_t* out_argmax;     /* [B*L] greedy candidate of every position        */
+  int32_t* out_ncommit;    /* [B] number of positions committed this step     */
+  int32_t* out_commit_pos; /* [B*block_len] committed positions of sequence b,
+                              ascending, in row b, padded with -1             */
+  int32_t rule;            /* FORK_RULE_*; fork_step uses FORK_RULE_LEFTMOST  */
+  /* Caller-provided device workspace (NULL = library-managed).  Must hold
+     fork_workspace_bytes(B, L, V) bytes and be 256-byte aligned. */
+  void* workspace;
+  size_t workspace_bytes;
+  /* Optional profiling hooks (NULL = none): hipEvent_t handles recorded on
+     `stream` immediately before and after the LM-head kernel, so a caller
+     can time that kernel alone with hipEventElapsedTime. */
+  void* ev_lmhead_begin;
+  void* ev_lmhead_end;
+} fork_step_args;
+
+/* fork_step with the extras above.  Same return codes. */
+int fork_step_ex(const fork_step_args* args);
+
+/* Device workspace bytes a step with these sizes needs (per-tile partial
+   statistics and the per-position candidates); 0 if the sizes are invalid. */
+size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
+
+/* Description of the last non-OK return on the calling thread ("" if none).
+   The string stays valid until the thread's next call into the library. */
+const char* fork_last_error(void);
+
+/* Free the library-managed workspaces of every device.  Must not race with
+   work still using them (synchronise first). */
+void fork_release(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int fork_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FORK_STEP_H */

@@ -16,10 +16,9 @@ __all__ = ["fork_step", "fork_step_ex", "workspace_bytes", "release", "version",
 
 
 def __getattr__(name):
+    import importlib
     if name in ("fork_step", "fork_step_ex", "workspace_bytes", "release", "version", "lib"):
-        from . import _binding
-        return getattr(_binding, name)
+        return getattr(importlib.import_module("._binding", __name__), name)
     if name == "synth":
-        from . import synth
-        return synth
+        return importlib.import_module(".synth", __name__)
     raise AttributeError(name)

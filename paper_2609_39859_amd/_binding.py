@@ -1,0 +1,187 @@
+"""ctypes binding of libforkstep.so (the C ABI in include/fork_step.h).
+
+Argument marshalling only: shapes, dtypes, devices and contiguity are checked,
+then raw device pointers and the current HIP stream are handed to the library,
+where every step of the computation runs in HIP kernels.  There is no CPU or
+PyTorch fallback: if the library is missing the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libforkstep.so")
+
+FORK_OK = 0
+FORK_EINVAL = -1
+FORK_EUNSUPPORTED = -2
+FORK_EHIP = -3
+FORK_ENOMEM = -4
+FORK_BF16 = 0
+FORK_F32 = 1
+FORK_RULE_LEFTMOST = 0
+FORK_RULE_MAXCONF = 1
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+
+
+class ForkStepArgs(ctypes.Structure):
+    _fields_ = [
+        ("hidden", _P), ("W_head", _P), ("tokens", _P), ("mask", _P),
+        ("block_start", _P), ("block_len", _I32), ("tau", ctypes.c_float),
+        ("out_conf", _P), ("out_entropy", _P), ("out_logp", _P),
+        ("out_fallback", _P),
+        ("B", _I32), ("L", _I32), ("d", _I32), ("V", _I32), ("dtype", _I32),
+        ("stream", _P),
+        ("out_lse", _P), ("out_argmax", _P), ("out_ncommit", _P),
+        ("out_commit_pos", _P), ("rule", _I32),
+        ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
+        ("ev_lmhead_begin", _P), ("ev_lmhead_end", _P),
+    ]
+
+
+class ForkError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("fork_step failed (%d): %s" % (code, msg))
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Load libforkstep.so (after torch, so that the HIP runtime torch already
+    loaded is the one the library binds to)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libforkstep.so is not built (expected at %s); run "
+                "`python -c 'import __graft_entry__ as g; g.build()'` or "
+                "`python -m paper_2609_39859_amd.build`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        L.fork_step.restype = ctypes.c_int
+        L.fork_step.argtypes = [_P, _P, _P, _P, _P, _I32, ctypes.c_float, _P, _P,
+                                _P, _P, _I32, _I32, _I32, _I32, _I32, _P]
+        L.fork_step_ex.restype = ctypes.c_int
+        L.fork_step_ex.argtypes = [ctypes.POINTER(ForkStepArgs)]
+        L.fork_workspace_bytes.restype = ctypes.c_size_t
+        L.fork_workspace_bytes.argtypes = [_I32, _I32, _I32]
+        L.fork_last_error.restype = ctypes.c_char_p
+        L.fork_last_error.argtypes = []
+        L.fork_release.restype = None
+        L.fork_release.argtypes = []
+        L.fork_version.restype = ctypes.c_int
+        L.fork_version.argtypes = []
+        _lib = L
+    return _lib
+
+
+def _check(t: torch.Tensor, name: str, dtype, numel: int, device) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (name, t.numel(), numel))
+    return t.data_ptr()
+
+
+def _opt(t: Optional[torch.Tensor], name, dtype, numel, device):
+    return None if t is None else _check(t, name, dtype, numel, device)
+
+
+def _stream_handle(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream
+
+
+def fork_step(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tensor,
+              mask: torch.Tensor, block_start: torch.Tensor, block_len: int,
+              tau: float, out_conf: torch.Tensor, out_entropy: torch.Tensor,
+              out_logp: torch.Tensor, out_fallback: torch.Tensor, *,
+              B: int, L: int, stream=None) -> None:
+    """One denoising step on the GPU (see include/fork_step.h, fork_step)."""
+    fork_step_ex(hidden, W_head, tokens, mask, block_start, block_len, tau,
+                 out_conf, out_entropy, out_logp, out_fallback, B=B, L=L,
+                 stream=stream)
+
+
+def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tensor,
+                 mask: torch.Tensor, block_start: torch.Tensor, block_len: int,
+                 tau: float, out_conf: torch.Tensor, out_entropy: torch.Tensor,
+                 out_logp: torch.Tensor, out_fallback: torch.Tensor, *,
+                 B: int, L: int, out_lse=None, out_argmax=None, out_ncommit=None,
+                 out_commit_pos=None, rule: int = FORK_RULE_LEFTMOST,
+                 workspace: Optional[torch.Tensor] = None, stream=None,
+                 events=None) -> None:
+    """fork_step_ex of the C ABI; optional outputs may be None.  ``events``
+    is an optional pair of raw hipEvent_t handles (ints) recorded around the
+    LM-head kernel."""
+    if hidden.dim() != 2 or W_head.dim() != 2:
+        raise ValueError("hidden and W_head must be 2-D")
+    device = hidden.device
+    if device.type != "cuda":
+        raise ValueError("fork_step runs on the GPU; hidden is on %s" % device)
+    M, d = hidden.shape
+    V = W_head.shape[0]
+    if M != B * L:
+        raise ValueError("hidden has %d rows, expected B*L = %d" % (M, B * L))
+    if hidden.dtype == torch.bfloat16:
+        dt = FORK_BF16
+    elif hidden.dtype == torch.float32:
+        dt = FORK_F32
+    else:
+        raise TypeError("hidden must be bfloat16 or float32")
+    a = ForkStepArgs()
+    a.hidden = _check(hidden, "hidden", hidden.dtype, M * d, device)
+    a.W_head = _check(W_head, "W_head", hidden.dtype, V * d, device)
+    a.tokens = _check(tokens, "tokens", torch.int32, M, device)
+    a.mask = _check(mask, "mask", torch.uint8, M, device)
+    a.block_start = _check(block_start, "block_start", torch.int32, B, device)
+    a.block_len = int(block_len)
+    a.tau = float(tau)
+    a.out_conf = _check(out_conf, "out_conf", torch.float32, M, device)
+    a.out_entropy = _check(out_entropy, "out_entropy", torch.float32, M, device)
+    a.out_logp = _check(out_logp, "out_logp", torch.float32, M, device)
+    a.out_fallback = _check(out_fallback, "out_fallback", torch.int32, B, device)
+    a.B, a.L, a.d, a.V, a.dtype = B, L, d, V, dt
+    a.stream = _stream_handle(stream, device)
+    a.out_lse = _opt(out_lse, "out_lse", torch.float32, M, device)
+    a.out_argmax = _opt(out_argmax, "out_argmax", torch.int32, M, device)
+    a.out_ncommit = _opt(out_ncommit, "out_ncommit", torch.int32, B, device)
+    a.out_commit_pos = _opt(out_commit_pos, "out_commit_pos", torch.int32,
+                            B * int(block_len), device)
+    a.rule = int(rule)
+    if workspace is not None:
+        if workspace.device != device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on %s" % device)
+        a.workspace = workspace.data_ptr()
+        a.workspace_bytes = workspace.numel() * workspace.element_size()
+    if events is not None:
+        a.ev_lmhead_begin, a.ev_lmhead_end = events
+    rc = lib().fork_step_ex(ctypes.byref(a))
+    if rc != FORK_OK:
+        raise ForkError(rc, lib().fork_last_error().decode())
+
+
+def workspace_bytes(B: int, L: int, V: int) -> int:
+    return int(lib().fork_workspace_bytes(B, L, V))
+
+
+def release() -> None:
+    lib().fork_release()
+
+
+def version() -> int:
+    return int(lib().fork_version())

@@ -1,0 +1,215 @@
+// C ABI of the Fork-dLLM step (declared in include/fork_step.h): argument
+// validation, the library-managed workspace, and the three launches
+//   gemm_stats (LM head + per-tile statistics) -> merge -> select
+// enqueued on the caller's stream.
+#include "fork_step.h"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <mutex>
+#include <vector>
+
+#include "fork_kernels.h"
+
+namespace {
+
+constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
+constexpr size_t kAlign = 256;
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Workspace layout: [partials: nvt*M float4][argmax: M int32].
+struct Layout {
+  size_t partial_off, argmax_off, total;
+};
+
+bool layout_for(int32_t B, int32_t L, int32_t V, Layout* out) {
+  if (B <= 0 || L <= 0 || V <= 0) return false;
+  const long long M = (long long)B * L;
+  if (M > 0x7fffffffLL) return false;
+  const size_t nvt = (size_t)fork::num_vocab_tiles(V);
+  out->partial_off = 0;
+  out->argmax_off = align_up(nvt * (size_t)M * sizeof(float4));
+  out->total = out->argmax_off + align_up((size_t)M * sizeof(int32_t));
+  return true;
+}
+
+struct DeviceWorkspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_ws_mutex;
+std::vector<DeviceWorkspace> g_ws;  // indexed by device ordinal
+
+int get_workspace(size_t need, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(FORK_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  if ((int)g_ws.size() <= dev) g_ws.resize(dev + 1);
+  DeviceWorkspace& ws = g_ws[dev];
+  if (ws.bytes < need) {
+    if (ws.ptr) {
+      // hipFree waits for work still using the old buffer
+      e = hipFree(ws.ptr);
+      ws.ptr = nullptr;
+      ws.bytes = 0;
+      if (e != hipSuccess) return fail(FORK_EHIP, "hipFree: %s", hipGetErrorString(e));
+    }
+    void* p = nullptr;
+    e = hipMalloc(&p, need);
+    if (e != hipSuccess || !p)
+      return fail(FORK_ENOMEM, "hipMalloc(%zu) for the workspace: %s", need, hipGetErrorString(e));
+    ws.ptr = p;
+    ws.bytes = need;
+  }
+  *out = ws.ptr;
+  return FORK_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int validate(const fork_step_args* a) {
+  if (!a) return fail(FORK_EINVAL, "args is NULL");
+  if (!a->hidden || !a->W_head || !a->tokens || !a->mask || !a->block_start || !a->out_conf ||
+      !a->out_entropy || !a->out_logp || !a->out_fallback)
+    return fail(FORK_EINVAL, "a required pointer is NULL");
+  if (a->B <= 0 || a->L <= 0 || a->d <= 0 || a->V <= 0)
+    return fail(FORK_EINVAL, "sizes must be positive (B=%d L=%d d=%d V=%d)", a->B, a->L, a->d, a->V);
+  if ((long long)a->B * a->L > 0x7fffffffLL)
+    return fail(FORK_EINVAL, "B*L = %lld does not fit int32", (long long)a->B * a->L);
+  if (a->block_len <= 0 || a->block_len > a->L)
+    return fail(FORK_EINVAL, "block_len=%d must lie in [1, L=%d]", a->block_len, a->L);
+  if (!isfinite(a->tau)) return fail(FORK_EINVAL, "tau must be finite");
+  if (a->dtype != FORK_BF16 && a->dtype != FORK_F32)
+    return fail(FORK_EINVAL, "unknown dtype %d", a->dtype);
+  if (a->rule != FORK_RULE_LEFTMOST && a->rule != FORK_RULE_MAXCONF)
+    return fail(FORK_EINVAL, "unknown fallback rule %d", a->rule);
+  if (a->dtype == FORK_BF16 && a->d % 8 != 0)
+    return fail(FORK_EUNSUPPORTED, "bf16 path needs d %% 8 == 0 (d=%d)", a->d);
+  if (a->dtype == FORK_F32 && a->d % 4 != 0)
+    return fail(FORK_EUNSUPPORTED, "fp32 path needs d %% 4 == 0 (d=%d)", a->d);
+  if (!aligned16(a->hidden) || !aligned16(a->W_head))
+    return fail(FORK_EINVAL, "hidden and W_head must be 16-byte aligned");
+  return FORK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fork_step_ex(const fork_step_args* a) {
+  int rc = validate(a);
+  if (rc != FORK_OK) return rc;
+  Layout lay;
+  if (!layout_for(a->B, a->L, a->V, &lay)) return fail(FORK_EINVAL, "invalid sizes");
+  void* ws = a->workspace;
+  if (ws) {
+    if (a->workspace_bytes < lay.total)
+      return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, lay.total);
+    if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
+  } else {
+    rc = get_workspace(lay.total, &ws);
+    if (rc != FORK_OK) return rc;
+  }
+  const int M = a->B * a->L;
+  const int nvt = fork::num_vocab_tiles(a->V);
+  float4* partials = reinterpret_cast<float4*>(static_cast<char*>(ws) + lay.partial_off);
+  int32_t* argmax = a->out_argmax ? a->out_argmax
+                                  : reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.argmax_off);
+  hipStream_t stream = static_cast<hipStream_t>(a->stream);
+
+  hipError_t e;
+  if (a->ev_lmhead_begin) {
+    e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_begin), stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  e = fork::launch_gemm_stats(a->hidden, a->W_head, a->dtype == FORK_BF16, M, a->d, a->V,
+                              partials, stream);
+  if (e != hipSuccess) return fail(FORK_EHIP, "gemm_stats launch: %s", hipGetErrorString(e));
+  if (a->ev_lmhead_end) {
+    e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_end), stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  e = fork::launch_merge(partials, M, nvt, a->out_conf, a->out_entropy, a->out_logp, a->out_lse,
+                         argmax, stream);
+  if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
+  e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf, argmax,
+                          a->tokens, a->mask, a->block_start, a->out_fallback, a->out_ncommit,
+                          a->out_commit_pos, stream);
+  if (e != hipSuccess) return fail(FORK_EHIP, "select launch: %s", hipGetErrorString(e));
+
+  static const bool sync_each = [] {
+    const char* s = getenv("FORK_SYNC");
+    return s && s[0] == '1';
+  }();
+  if (sync_each) {
+    e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "step failed: %s", hipGetErrorString(e));
+  }
+  return FORK_OK;
+}
+
+int fork_step(const void* hidden, const void* W_head, int32_t* tokens, uint8_t* mask,
+              int32_t* block_start, int32_t block_len, float tau, float* out_conf,
+              float* out_entropy, float* out_logp, int32_t* out_fallback, int32_t B, int32_t L,
+              int32_t d, int32_t V, int32_t dtype, void* stream) {
+  fork_step_args a = {};
+  a.hidden = hidden;
+  a.W_head = W_head;
+  a.tokens = tokens;
+  a.mask = mask;
+  a.block_start = block_start;
+  a.block_len = block_len;
+  a.tau = tau;
+  a.out_conf = out_conf;
+  a.out_entropy = out_entropy;
+  a.out_logp = out_logp;
+  a.out_fallback = out_fallback;
+  a.B = B;
+  a.L = L;
+  a.d = d;
+  a.V = V;
+  a.dtype = dtype;
+  a.stream = stream;
+  a.rule = FORK_RULE_LEFTMOST;
+  return fork_step_ex(&a);
+}
+
+size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V) {
+  Layout lay;
+  return layout_for(B, L, V, &lay) ? lay.total : 0;
+}
+
+const char* fork_last_error(void) { return g_err; }
+
+void fork_release(void) {
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  int cur = 0;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  for (size_t dev = 0; dev < g_ws.size(); ++dev) {
+    if (!g_ws[dev].ptr) continue;
+    if (hipSetDevice((int)dev) == hipSuccess) (void)hipFree(g_ws[dev].ptr);
+    g_ws[dev] = DeviceWorkspace();
+  }
+  if (have_cur) (void)hipSetDevice(cur);
+}
+
+int fork_version(void) { return kVersion; }
+
+}  // extern "C"

@@ -1,0 +1,46 @@
+// Internal interface between the C-ABI host code and the HIP kernels of the
+// Fork-dLLM step.  Not installed; the public interface is include/fork_step.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fork {
+
+// Vocabulary rows and positions covered by one GEMM workgroup.
+constexpr int kTileV = 256;
+constexpr int kTileP = 256;
+
+// Partial statistics of one position over one vocabulary tile, stored as a
+// float4 {m, s, t, idx}: m = max logit, s = sum exp(z - m),
+// t = sum exp(z - m) * (z - m), idx = lowest vocabulary index with z == m
+// (bit pattern of an int32).  An empty partial has s == 0.
+struct Partial {
+  float m, s, t;
+  int idx;
+};
+
+inline int num_vocab_tiles(int V) { return (V + kTileV - 1) / kTileV; }
+inline int num_pos_tiles(int M) { return (M + kTileP - 1) / kTileP; }
+
+// Logits of rows [0, M) of hidden against W (never stored) reduced to one
+// Partial per (vocabulary tile, position): partials[vt * M + r].
+hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16,
+                             int M, int d, int V, float4* partials,
+                             hipStream_t stream);
+
+// Merge the partials of each position over all vocabulary tiles into the
+// per-position results.  lse may be null.
+hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
+                        float* entropy, float* logp, float* lse,
+                        int32_t* argmax, hipStream_t stream);
+
+// Unmasking rule per sequence, in place.  ncommit / commit_pos may be null.
+hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
+                         const float* conf, const int32_t* argmax,
+                         int32_t* tokens, uint8_t* mask, int32_t* block_start,
+                         int32_t* fallback, int32_t* ncommit,
+                         int32_t* commit_pos, hipStream_t stream);
+
+}  // namespace fork

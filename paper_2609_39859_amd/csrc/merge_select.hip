@@ -1,0 +1,210 @@
+// Cross-tile merge of the per-tile statistics, and the unmasking rule.
+//
+// Merge (per position, over vocabulary tiles j):
+//   m = max_j m_j,  s = sum_j s_j e^(m_j - m),
+//   t = sum_j e^(m_j - m) (t_j + (m_j - m) s_j)
+// which is the exact re-basing of each tile's sums from its own maximum m_j to
+// the global one.  With q_v = e^(z_v - m) / s this gives
+//   confidence q(argmax) = 1/s,  log q(argmax) = -log s,
+//   log-normaliser = m + log s,  entropy = -sum q log q = log s - t/s,
+// the quantities of Section 2 (confidence), Section 3.1 (entropy) and
+// Section 3.2 (log-probability inside the ForkGRPO ratio) of the Fork-dLLM
+// paper.  The merge order is fixed, so results are bit-reproducible.
+//
+// Selection (Algorithm 2 of the paper, in the active block of the
+// semi-autoregressive regime of Section 4.1): one wave64 per sequence; the
+// threshold test is a ballot over the block's lanes, the fallback is the
+// first set bit of the mask ballot (leftmost masked position), and committed
+// positions are compacted with a lane-prefix count.
+#include "fork_kernels.h"
+
+#include <math.h>
+
+namespace fork {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMergeRows = 64;    // positions per merge workgroup (one per lane)
+constexpr int kMergeWaves = 16;   // waves splitting the vocabulary tiles
+
+__device__ __forceinline__ float4 merge2(float4 a, float4 b) {
+  if (b.y == 0.f) return a;
+  if (a.y == 0.f) return b;
+  const float m = fmaxf(a.x, b.x);
+  const float ea = exp2f((a.x - m) * kLog2e), eb = exp2f((b.x - m) * kLog2e);
+  float4 r;
+  r.x = m;
+  r.y = a.y * ea + b.y * eb;
+  r.z = ea * (a.z + (a.x - m) * a.y) + eb * (b.z + (b.x - m) * b.y);
+  const int ia = __float_as_int(a.w), ib = __float_as_int(b.w);
+  const bool take_a = (a.x > b.x) || (a.x == b.x && ia < ib);
+  r.w = __int_as_float(take_a ? ia : ib);
+  return r;
+}
+
+__global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
+    const float4* __restrict__ partials, int M, int nvt, float* __restrict__ conf,
+    float* __restrict__ entropy, float* __restrict__ logp, float* __restrict__ lse,
+    int32_t* __restrict__ argmax) {
+  __shared__ float4 red[kMergeWaves][kMergeRows];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int r = blockIdx.x * kMergeRows + lane;
+  float4 acc = make_float4(-INFINITY, 0.f, 0.f, __int_as_float(0x7fffffff));
+  if (r < M)
+    for (int j = w; j < nvt; j += kMergeWaves)
+      acc = merge2(acc, partials[(size_t)j * M + r]);
+  red[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && r < M) {
+#pragma unroll
+    for (int k = 1; k < kMergeWaves; ++k) acc = merge2(acc, red[k][lane]);
+    const float log_s = logf(acc.y);
+    conf[r] = 1.0f / acc.y;
+    logp[r] = -log_s;
+    entropy[r] = log_s - acc.z / acc.y;
+    if (lse) lse[r] = acc.x + log_s;
+    argmax[r] = __float_as_int(acc.w);
+  }
+}
+
+__device__ __forceinline__ unsigned long long ballot(bool p) { return __ballot(p); }
+
+__global__ __launch_bounds__(64) void select_kernel(
+    int L, int BL, float tau, int rule, const float* __restrict__ conf,
+    const int32_t* __restrict__ argmax, int32_t* __restrict__ tokens,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ block_start,
+    int32_t* __restrict__ fallback, int32_t* __restrict__ ncommit,
+    int32_t* __restrict__ commit_pos) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const size_t base = (size_t)b * L;
+  int32_t* my_commits = commit_pos ? commit_pos + (size_t)b * BL : nullptr;
+
+  int s = block_start[b];
+  int status = 0;
+  if (s < 0 || s > L) {
+    status = -2;
+  } else {
+    // skip forward to the first block holding a masked position
+    bool found = false;
+    while (s < L) {
+      const int e = min(s + BL, L);
+      for (int c = s; c < e; c += 64) {
+        const int k = c + lane;
+        if (ballot(k < e && mask[base + k] != 0)) {
+          found = true;
+          break;
+        }
+      }
+      if (found) break;
+      s += BL;
+    }
+    if (!found) status = -1;
+  }
+  if (status != 0) {
+    if (lane == 0) {
+      fallback[b] = status;
+      if (ncommit) ncommit[b] = 0;
+    }
+    if (my_commits)
+      for (int i = lane; i < BL; i += 64) my_commits[i] = -1;
+    return;
+  }
+
+  const int e = min(s + BL, L);
+  // threshold set U = { k masked : conf[k] > tau }
+  int npass = 0;
+  for (int c = s; c < e; c += 64) {
+    const int k = c + lane;
+    const bool pass = k < e && mask[base + k] != 0 && conf[base + k] > tau;
+    npass += __popcll(ballot(pass));
+  }
+  const bool fb = npass == 0;
+  int pick = -1;
+  if (fb) {
+    if (rule == 0) {
+      // leftmost masked position of the block
+      for (int c = s; c < e; c += 64) {
+        const int k = c + lane;
+        const unsigned long long bm = ballot(k < e && mask[base + k] != 0);
+        if (bm) {
+          pick = c + __ffsll((long long)bm) - 1;
+          break;
+        }
+      }
+    } else {
+      // highest confidence, lowest position on ties
+      float best = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int c = s; c < e; c += 64) {
+        const int k = c + lane;
+        if (k < e && mask[base + k] != 0) {
+          const float v = conf[base + k];
+          if (bi == 0x7fffffff || v > best) {
+            best = v;
+            bi = k;
+          }
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ob = __shfl_xor(best, off);
+        const int oi = __shfl_xor(bi, off);
+        if (oi != 0x7fffffff && (bi == 0x7fffffff || ob > best || (ob == best && oi < bi))) {
+          best = ob;
+          bi = oi;
+        }
+      }
+      pick = bi;
+    }
+  }
+  // commit, compacting the committed positions in ascending order
+  int written = 0;
+  for (int c = s; c < e; c += 64) {
+    const int k = c + lane;
+    const bool masked = k < e && mask[base + k] != 0;
+    const bool commit = masked && (fb ? (k == pick) : (conf[base + k] > tau));
+    const unsigned long long bm = ballot(commit);
+    if (commit) {
+      tokens[base + k] = argmax[base + k];
+      mask[base + k] = 0;
+      if (my_commits) {
+        const unsigned long long below = bm & ((1ull << lane) - 1ull);
+        my_commits[written + __popcll(below)] = k;
+      }
+    }
+    written += __popcll(bm);
+  }
+  if (my_commits)
+    for (int i = written + lane; i < BL; i += 64) my_commits[i] = -1;
+  if (lane == 0) {
+    fallback[b] = fb ? 1 : 0;
+    block_start[b] = s;
+    if (ncommit) ncommit[b] = written;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
+                        float* entropy, float* logp, float* lse, int32_t* argmax,
+                        hipStream_t stream) {
+  const dim3 grid((unsigned)((M + kMergeRows - 1) / kMergeRows));
+  const dim3 block(kMergeRows * kMergeWaves);
+  hipLaunchKernelGGL(merge_kernel, grid, block, 0, stream, partials, M, nvt, conf,
+                     entropy, logp, lse, argmax);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
+                         const float* conf, const int32_t* argmax, int32_t* tokens,
+                         uint8_t* mask, int32_t* block_start, int32_t* fallback,
+                         int32_t* ncommit, int32_t* commit_pos, hipStream_t stream) {
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)B), dim3(64), 0, stream, L,
+                     block_len, tau, rule, conf, argmax, tokens, mask, block_start,
+                     fallback, ncommit, commit_pos);
+  return hipGetLastError();
+}
+
+}  // namespace fork

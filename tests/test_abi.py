@@ -1,0 +1,105 @@
+"""The C-ABI library loads and exports every symbol its header declares, and
+rejects bad arguments on the host before touching a GPU (no compute here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_39859_amd import _binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fork_step.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*(fork_[a-z_]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared_functions()
+    for n in ("fork_step", "fork_step_ex", "fork_workspace_bytes", "fork_last_error",
+              "fork_release", "fork_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_binding.LIB_PATH)
+    for n in _declared_functions():
+        assert hasattr(lib, n), "libforkstep.so does not export %s" % n
+
+
+def test_exports_are_c_symbols():
+    nm = os.popen("nm -D --defined-only %s" % _binding.LIB_PATH).read()
+    for n in _declared_functions():
+        assert re.search(r"\bT %s$" % n, nm, flags=re.M), n
+
+
+def test_version_and_workspace_sizes():
+    L = _binding.lib()
+    assert L.fork_version() == 10000
+    # per-tile partials (16 B per position per 256-entry vocabulary tile,
+    # padded to 256 B) + candidates (4 B per position, padded)
+    def expect(B, Lq, V):
+        M = B * Lq
+        nvt = (V + 255) // 256
+        pad = lambda x: (x + 255) // 256 * 256
+        return pad(nvt * M * 16) + pad(M * 4)
+    for B, Lq, V in [(1, 64, 1024), (4, 256, 32000), (8, 512, 126464), (3, 37, 1013)]:
+        assert L.fork_workspace_bytes(B, Lq, V) == expect(B, Lq, V)
+    assert L.fork_workspace_bytes(0, 5, 5) == 0
+    assert L.fork_workspace_bytes(5, 5, -1) == 0
+    assert L.fork_workspace_bytes(1 << 16, 1 << 16, 5) == 0
+
+
+def _args(**kw):
+    a = _binding.ForkStepArgs()
+    good = dict(hidden=16, W_head=32, tokens=48, mask=64, block_start=80, block_len=4,
+                tau=0.9, out_conf=96, out_entropy=112, out_logp=128, out_fallback=144,
+                B=2, L=8, d=16, V=100, dtype=_binding.FORK_BF16, rule=0)
+    good.update(kw)
+    for k, v in good.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hidden=0), _binding.FORK_EINVAL),
+    (dict(out_fallback=0), _binding.FORK_EINVAL),
+    (dict(B=0), _binding.FORK_EINVAL),
+    (dict(V=-3), _binding.FORK_EINVAL),
+    (dict(block_len=0), _binding.FORK_EINVAL),
+    (dict(block_len=9), _binding.FORK_EINVAL),
+    (dict(tau=float("nan")), _binding.FORK_EINVAL),
+    (dict(tau=float("inf")), _binding.FORK_EINVAL),
+    (dict(dtype=7), _binding.FORK_EINVAL),
+    (dict(rule=5), _binding.FORK_EINVAL),
+    (dict(d=12), _binding.FORK_EUNSUPPORTED),
+    (dict(d=6, dtype=_binding.FORK_F32), _binding.FORK_EUNSUPPORTED),
+    (dict(hidden=18), _binding.FORK_EINVAL),
+    (dict(B=1 << 16, L=1 << 16), _binding.FORK_EINVAL),
+    (dict(workspace=256, workspace_bytes=10), _binding.FORK_EINVAL),
+    (dict(workspace=250, workspace_bytes=1 << 30), _binding.FORK_EINVAL),
+])
+def test_bad_arguments_rejected_on_host(kw, code):
+    """Validation runs before any HIP call; the pointers here are never
+    dereferenced."""
+    L = _binding.lib()
+    a = _args(**kw)
+    assert L.fork_step_ex(ctypes.byref(a)) == code
+    assert L.fork_last_error().decode() != ""
+
+
+def test_null_args_struct():
+    L = _binding.lib()
+    assert L.fork_step_ex(None) == _binding.FORK_EINVAL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        _binding.fork_step(x, x, None, None, None, 1, 0.5, None, None, None, None, B=1, L=4)

@@ -1,0 +1,357 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the
+same seeded input bits (see tests/harness.py for the comparison rules).
+
+Small workloads are checked on every row and, for decodes, in lock-step:
+each step starts both sides from the oracle's state.  Full-size workloads
+(d = 4096, V = 126464) are checked in the launch configuration the benchmark
+times, on sampled rows the oracle evaluates one by one, plus properties that
+hold for every row.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39859_amd import _binding, synth
+
+from harness import (Report, check_rule_on_own_stats, compare_decisions, compare_stats,
+                     gpu_step, host_bits)
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _lam(cfg_tau):
+    return float(np.float32(cfg_tau))
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None):
+    """Decode cfg in lock-step; rows_fn(step, mask, block_start) picks the rows
+    the oracle evaluates (default: all).  Returns the report."""
+    W = synth.weights(cfg)
+    Wd = W.to(DEV)
+    Wb = host_bits(W)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    B, L, BL = cfg.B, cfg.L, cfg.block_len
+    rep = Report()
+    t = 0
+    while msk[:].any() and (max_steps is None or t < max_steps):
+        h = synth.hidden(cfg, t, W=W)
+        hb = host_bits(h)
+        rows = np.arange(cfg.M) if rows_fn is None else rows_fn(t, msk, bs)
+        ref = oracle.row_stats(hb, Wb, rows)
+        g = gpu_step(h.to(DEV), Wd, tok, msk, bs, B, L, BL, cfg.tau, rule=rule)
+        ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
+        conf_full = np.full(cfg.M, np.nan)
+        am_full = np.zeros(cfg.M, np.int32)
+        conf_full[rows] = ref["conf"]
+        am_full[rows] = ref["argmax"]
+        sel = oracle.select(conf_full, am_full, tok, msk, bs, B, L, BL, _lam(cfg.tau), rule)
+        compare_decisions(g, sel, conf_full, tok, msk, bs, B, L, BL, cfg.tau, rep,
+                          rule=rule, near_tie_rows=ties)
+        tok, msk, bs = sel[0], sel[1], sel[2]
+        t += 1
+        assert t <= cfg.G + 1
+    _say("%s: %d steps, %d rows (%d near-tie), %d sequence-steps (%d near-threshold), max err %s"
+         % (cfg.name, t, rep.rows, rep.near_tie_rows, rep.seqs, rep.near_threshold_seqs,
+            {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    return rep, t
+
+
+def _active_rows(cfg, msk, bs):
+    rows = []
+    for b in range(cfg.B):
+        masked = [k for k in range(int(bs[b]), cfg.L) if msk[b * cfg.L + k]]
+        if masked:
+            s = int(bs[b]) + ((masked[0] - int(bs[b])) // cfg.block_len) * cfg.block_len
+            rows += [b * cfg.L + k for k in range(s, min(s + cfg.block_len, cfg.L))]
+    return np.array(sorted(set(rows)), np.int64)
+
+
+# ------------------------------------------------------------ small workloads
+
+def test_crafted_ties_and_layout():
+    """One-hot hidden rows against a periodic one-hot W: z_v = 3 exactly for
+    every v congruent to the row's hot index, 0 elsewhere.  The candidate must
+    be the lowest tied index (checks the accumulator layout and the tie-break
+    across lanes, waves and vocabulary tiles); conf = 1/(k + (V-k) e^-3)."""
+    _need_gpu()
+    for dtype in (torch.float32, torch.bfloat16):
+        d, V, B, L = 64, 1000, 3, 50
+        M = B * L
+        hot = (np.arange(M) * 7) % d
+        h = torch.zeros(M, d)
+        h[torch.arange(M), torch.as_tensor(hot)] = 3.0
+        W = torch.zeros(V, d)
+        W[torch.arange(V), torch.arange(V) % d] = 1.0
+        h, W = h.to(dtype), W.to(dtype)
+        tok = np.zeros(M, np.int32)
+        msk = np.zeros(M, np.uint8)
+        bs = np.zeros(B, np.int32)
+        g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, B, L, 10, 0.5)
+        assert np.array_equal(g.argmax, hot)
+        k = np.array([len(range(x, V, d)) for x in hot])
+        conf = 1.0 / (k + (V - k) * math.exp(-3.0))
+        np.testing.assert_allclose(g.conf, conf, atol=2e-6, rtol=1e-5)
+        ref = oracle.row_stats(host_bits(h), host_bits(W))
+        np.testing.assert_allclose(g.entropy, ref["entropy"], atol=2e-5)
+        np.testing.assert_allclose(g.logp, ref["logp"], atol=2e-5)
+        assert np.all(g.fallback == -1) and np.all(g.ncommit == 0)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_peaked"])
+def test_tiny_lockstep_decode(name):
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    rep, steps = lockstep_decode(cfg)
+    assert steps <= cfg.G
+    assert rep.near_threshold_seqs <= max(1, rep.seqs // 20)
+    assert rep.near_tie_rows <= max(1, rep.rows // 50)
+
+
+@pytest.mark.parametrize("lam", [0.0, 0.5, 1.0])
+def test_tiny_threshold_special_cases(lam):
+    """lambda = 0: whole blocks per step; lambda = 1: autoregressive order."""
+    _need_gpu()
+    cfg = synth.CONFIGS["tiny"].with_(tau=lam)
+    rep, steps = lockstep_decode(cfg)
+    if lam == 0.0:
+        assert steps == math.ceil(cfg.G / cfg.block_len)
+    if lam == 1.0:
+        assert steps == cfg.G
+
+
+def test_tiny_free_running_matches_oracle_decode():
+    """Without resynchronisation the GPU decode reproduces the oracle decode
+    (this workload has no near-threshold or near-tie events)."""
+    _need_gpu()
+    cfg = synth.CONFIGS["tiny"]
+    W = synth.weights(cfg)
+    Wd, Wb = W.to(DEV), host_bits(W)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    gt, gm, gb = tok.copy(), msk.copy(), bs.copy()
+    for t in range(cfg.G + 1):
+        if not msk.any():
+            break
+        h = synth.hidden(cfg, t)
+        st = oracle.step(host_bits(h), Wb, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, _lam(cfg.tau))
+        g = gpu_step(h.to(DEV), Wd, gt, gm, gb, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+        tok, msk, bs = st["tokens"], st["mask"], st["block_start"]
+        gt, gm, gb = g.tokens, g.mask, g.block_start
+        assert np.array_equal(g.fallback, st["fallback"])
+    assert not gm.any() and np.array_equal(gt, tok)
+
+
+def test_mid_step0_all_rows():
+    _need_gpu()
+    cfg = synth.CONFIGS["mid"]
+    W = synth.weights(cfg)
+    h = synth.hidden(cfg, 0)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    hb, Wb = host_bits(h), host_bits(W)
+    ref = oracle.row_stats(hb, Wb)
+    g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    rep = Report()
+    ties = compare_stats(g, ref, np.arange(cfg.M), hb, Wb, cfg.d, rep)
+    sel = oracle.select(ref["conf"], ref["argmax"], tok, msk, bs, cfg.B, cfg.L, cfg.block_len,
+                        _lam(cfg.tau))
+    compare_decisions(g, sel, ref["conf"], tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
+                      rep, near_tie_rows=ties)
+    _say("mid step 0: near-tie rows %d / %d, max err %s" % (rep.near_tie_rows, rep.rows, rep.max_err))
+    assert rep.near_tie_rows <= cfg.M // 50
+
+
+@pytest.mark.parametrize("rule", [_binding.FORK_RULE_LEFTMOST, _binding.FORK_RULE_MAXCONF])
+def test_mid_planted_lockstep_decode(rule):
+    """Planted confident rows force multi-commit parallel steps at
+    d = 1024, V = 32000; both fallback rules."""
+    _need_gpu()
+    cfg = synth.CONFIGS["mid_planted"]
+    rep, steps = lockstep_decode(cfg, rule=rule,
+                                 rows_fn=lambda t, m, b: _active_rows(cfg, m, b))
+    assert steps < 0.9 * 39  # parallel steps happen
+
+
+RAGGED = [
+    # B, L, d, V, dtype, block_len
+    (3, 37, 200, 1013, torch.bfloat16, 8),
+    (1, 1, 8, 1, torch.bfloat16, 1),
+    (2, 300, 72, 257, torch.float32, 300),
+    (5, 61, 520, 2049, torch.bfloat16, 7),
+    (2, 129, 1032, 777, torch.bfloat16, 64),
+    (1, 257, 96, 300, torch.float32, 65),
+]
+
+
+@pytest.mark.parametrize("B,L,d,V,dtype,BL", RAGGED)
+@pytest.mark.parametrize("rule", [0, 1])
+def test_ragged_shapes_and_random_states(B, L, d, V, dtype, BL, rule):
+    """Shapes that are not multiples of the tiles, random masks and block
+    starts (including idle sequences and block_start = L)."""
+    _need_gpu()
+    gen = torch.Generator().manual_seed(B * 1000 + L + d + V + rule)
+    M = B * L
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(dtype)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(dtype)
+    rng = np.random.default_rng(M + V)
+    msk = (rng.random(M) < 0.5).astype(np.uint8)
+    tok = np.where(msk, -1, rng.integers(0, V, M)).astype(np.int32)
+    bs = rng.integers(0, L + 1, B).astype(np.int32)
+    if B > 1:
+        msk[(B - 1) * L:] = 0  # an idle sequence
+    hb, Wb = host_bits(h), host_bits(W)
+    ref = oracle.row_stats(hb, Wb)
+    for tau in (0.05, 0.3):
+        g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, B, L, BL, tau, rule=rule)
+        rep = Report()
+        ties = compare_stats(g, ref, np.arange(M), hb, Wb, d, rep)
+        sel = oracle.select(ref["conf"], ref["argmax"], tok, msk, bs, B, L, BL, _lam(tau), rule)
+        compare_decisions(g, sel, ref["conf"], tok, msk, bs, B, L, BL, tau, rep, rule=rule,
+                          near_tie_rows=ties)
+
+
+def test_caller_workspace_and_determinism():
+    """Caller-provided workspace gives the same bits as the library one, and
+    repeated runs are bit-identical (fixed merge order, no atomics)."""
+    _need_gpu()
+    cfg = synth.CONFIGS["mid"]
+    W = synth.weights(cfg).to(DEV)
+    h = synth.hidden(cfg, 3).to(DEV)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    a = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    b = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    nbytes = _binding.workspace_bytes(cfg.B, cfg.L, cfg.V)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=DEV)
+    off = (-ws.data_ptr()) % 256
+    c = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
+                 workspace=ws[off:off + nbytes])
+    for x in (b, c):
+        for k in ("conf", "entropy", "logp", "lse"):
+            assert np.array_equal(getattr(a, k).view(np.int32), getattr(x, k).view(np.int32)), k
+        for k in ("argmax", "tokens", "mask", "block_start", "fallback", "ncommit", "commit_pos"):
+            assert np.array_equal(getattr(a, k), getattr(x, k)), k
+    with pytest.raises(_binding.ForkError):
+        gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
+                 workspace=ws[off:off + nbytes - 256])
+
+
+def test_bad_block_start_is_reported_in_data():
+    _need_gpu()
+    B, L, d, V = 3, 16, 16, 40
+    h = torch.randn(B * L, d).to(torch.bfloat16).to(DEV)
+    W = torch.randn(V, d).to(torch.bfloat16).to(DEV)
+    msk = np.ones(B * L, np.uint8)
+    tok = np.full(B * L, -1, np.int32)
+    bs = np.array([-1, 17, 16], np.int32)
+    g = gpu_step(h, W, tok, msk, bs, B, L, 4, 0.5)
+    assert g.fallback.tolist() == [-2, -2, -1]
+    assert np.array_equal(g.mask, msk) and np.array_equal(g.tokens, tok)
+    assert g.block_start.tolist() == [-1, 17, 16]
+    assert np.all(g.commit_pos == -1)
+
+
+# ------------------------------------------------------------- full sizes
+
+def _sample_rows(cfg, msk, bs, n_seq=4, n_random=32, seed=0):
+    rng = np.random.default_rng(seed)
+    act = _active_rows(cfg.with_(B=min(cfg.B, n_seq)), msk[: min(cfg.B, n_seq) * cfg.L], bs)
+    extra = rng.choice(cfg.M, n_random, replace=False)
+    edge = np.array([0, 255, 256, cfg.M - 1])
+    return np.array(sorted(set(act.tolist()) | set(extra.tolist()) | set(edge.tolist())), np.int64), \
+        list(range(min(cfg.B, n_seq)))
+
+
+@pytest.mark.parametrize("name", ["llada8b", "rollout", "long"])
+def test_full_size_step_sampled(name):
+    """One step at the benchmark's full sizes and launch configuration:
+    sampled rows against the oracle, decisions exact on the sequences whose
+    active block the oracle evaluated, and every-row properties:
+    0 <= H <= log V, 1/V <= conf <= 1, log q = -log(1/conf) within float
+    error.  With these distributions no position is confident (max q is far
+    below lambda), so every sequence takes a fallback step at position P."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    _say("full-size %s: generating inputs" % name)
+    W = synth.weights(cfg, device=DEV)
+    h = synth.hidden(cfg, 0, device=DEV)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    _say("full-size %s: GPU step" % name)
+    g = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    rows, seqs = _sample_rows(cfg, msk, bs)
+    _say("full-size %s: oracle on %d rows" % (name, rows.size))
+    hb, Wb = host_bits(h), host_bits(W)
+    ref = oracle.row_stats(hb, Wb, rows)
+    rep = Report()
+    ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
+    conf_full = np.full(cfg.M, np.nan)
+    am_full = np.zeros(cfg.M, np.int32)
+    conf_full[rows] = ref["conf"]
+    am_full[rows] = ref["argmax"]
+    sel = oracle.select(conf_full, am_full, tok, msk, bs, cfg.B, cfg.L, cfg.block_len,
+                        _lam(cfg.tau))
+    compare_decisions(g, sel, conf_full, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
+                      rep, seqs=seqs, near_tie_rows=ties)
+    check_rule_on_own_stats(g, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau, 0,
+                            range(cfg.B))
+    logV = math.log(cfg.V)
+    assert np.all(g.entropy >= -1e-3) and np.all(g.entropy <= logV + 1e-3)
+    assert np.all(g.conf >= (1.0 / cfg.V) * (1 - 1e-3)) and np.all(g.conf <= 1.0 + 1e-6)
+    np.testing.assert_allclose(g.logp, np.log(g.conf.astype(np.float64)), atol=1e-4)
+    assert np.all(g.fallback == 1)
+    assert np.all(g.commit_pos[:, 0] == cfg.P) and np.all(g.commit_pos[:, 1:] == -1)
+    _say("full-size %s: %d rows ok (%d near-tie), max err %s" % (
+        name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+
+
+@pytest.mark.parametrize("name", ["llada8b"])
+def test_full_size_decode_is_autoregressive(name):
+    """A whole decode at the full LLaDA-8B shape on the GPU: with no
+    confident position, every step is a fallback step and the commits follow
+    AR order P, P+1, ... (Section 2); a few steps are checked against the
+    oracle on their active rows."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    W = synth.weights(cfg, device=DEV)
+    Wb = None
+    tok, msk, bs = (x.to(DEV) for x in synth.initial_state(cfg))
+    B, L, BL, M = cfg.B, cfg.L, cfg.block_len, cfg.M
+    f32 = dict(dtype=torch.float32, device=DEV)
+    conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
+    am = torch.empty(M, dtype=torch.int32, device=DEV)
+    fb = torch.empty(B, dtype=torch.int32, device=DEV)
+    cp = torch.empty(B * BL, dtype=torch.int32, device=DEV)
+    check_steps = {0, 1, 31, 32, cfg.G - 1}
+    for t in range(cfg.G):
+        h = synth.hidden(cfg, t, device=DEV)
+        if t in check_steps:
+            before = msk.cpu().numpy()
+        _binding.fork_step_ex(h, W, tok, msk, bs, BL, cfg.tau, conf, ent, logp, fb, B=B, L=L,
+                              out_argmax=am, out_commit_pos=cp)
+        fbh = fb.cpu().numpy()
+        cph = cp.cpu().numpy().reshape(B, BL)
+        assert np.all(fbh == 1), "step %d: fallback %s" % (t, fbh)
+        assert np.all(cph[:, 0] == cfg.P + t) and np.all(cph[:, 1:] == -1)
+        if t in check_steps:
+            if Wb is None:
+                Wb = host_bits(W)
+            rows = np.array([b * L + cfg.P + t for b in range(B)])
+            ref = oracle.row_stats(host_bits(h), Wb, rows)
+            gam = am.cpu().numpy()[rows]
+            gtok = tok.cpu().numpy()[rows]
+            ok = (gam == ref["argmax"]) | (ref["gap"] < 2e-3)
+            assert np.all(ok) and np.array_equal(gtok, gam)
+            assert before[rows].all()
+            _say("decode %s step %d ok" % (name, t))
+    assert not msk.cpu().numpy().reshape(B, L)[:, cfg.P:].any()
