@@ -101,6 +101,9 @@ def main():
     ap.add_argument("--config", default="llada8b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a plain 1 GiB device copy (a known-size kernel for "
+                         "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -121,6 +124,16 @@ def main():
     B, L, BL, M, d, V = cfg.B, cfg.L, cfg.block_len, cfg.M, cfg.d, cfg.V
     print("bench: %s B=%d L=%d d=%d V=%d, generating inputs" % (cfg.name, B, L, d, V),
           file=sys.stderr, flush=True)
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        print("bench: ran 3 copies of 1 GiB (read 1 GiB + write 1 GiB each)",
+              file=sys.stderr, flush=True)
 
     W = synth.weights(cfg, device=dev)
     n_batches = 4
