@@ -215,7 +215,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
-                     "kernel": "gemm_stats_kernel<bf16> (LM head + per-tile statistics)",
+                     "kernel": "gemm_stats_bf16_kernel (LM head + per-tile statistics)",
                      "algorithmic_flops_per_launch": flops},
         "cpu_baseline": None,
     }

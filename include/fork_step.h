@@ -98,7 +98,7 @@ enum {
  * out_logp     [B*L] float: log q(candidate) for every position.
  * out_fallback [B] int32: FORK_STEP_* per sequence.
  * B, L, d, V   sizes, all >= 1, B*L < 2^31; d % 8 == 0 for FORK_BF16,
- *              d % 4 == 0 for FORK_F32.
+ *              d % 4 == 0 for FORK_F32, d <= 2^20 (else FORK_EUNSUPPORTED).
  * dtype        FORK_BF16 or FORK_F32.
  * stream       hipStream_t to enqueue on (NULL = default stream).
  *

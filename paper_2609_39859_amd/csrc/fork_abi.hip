@@ -19,6 +19,9 @@ namespace {
 
 constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
 constexpr size_t kAlign = 256;
+// Per-tile byte offsets of the LM-head kernel are 32-bit: 256 rows x d x 4 B
+// must stay below 2^31.
+constexpr int kMaxD = 1 << 20;
 
 thread_local char g_err[512] = "";
 
@@ -104,6 +107,8 @@ int validate(const fork_step_args* a) {
     return fail(FORK_EUNSUPPORTED, "bf16 path needs d %% 8 == 0 (d=%d)", a->d);
   if (a->dtype == FORK_F32 && a->d % 4 != 0)
     return fail(FORK_EUNSUPPORTED, "fp32 path needs d %% 4 == 0 (d=%d)", a->d);
+  if (a->d > kMaxD)
+    return fail(FORK_EUNSUPPORTED, "d=%d exceeds the supported maximum %d", a->d, kMaxD);
   if (!aligned16(a->hidden) || !aligned16(a->W_head))
     return fail(FORK_EINVAL, "hidden and W_head must be 16-byte aligned");
   return FORK_OK;

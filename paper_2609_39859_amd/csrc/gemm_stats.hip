@@ -11,23 +11,31 @@
 //   m   = max_v z_v                 idx = lowest v attaining m
 //   s   = sum_v exp(z_v - m)        t   = sum_v exp(z_v - m) * (z_v - m)
 //
-// Work decomposition (gfx950 / CDNA4):
+// Work decomposition (gfx950 / CDNA4), common to both element types:
 //   * one workgroup = 256 vocabulary rows x 256 positions, 8 wave64s laid out
 //     2 (vocabulary) x 4 (positions); each wave owns 128 x 64 outputs as
-//     4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulate);
+//     4 x 2 tiles of 32x32 MFMA accumulators (fp32);
 //   * the MFMA "A" operand is W (vocabulary on the MFMA M axis) and "B" is
 //     hidden, so each lane's accumulators hold 16 vocabulary values of ONE
 //     position: the vocabulary reduction is mostly in-lane, plus one
 //     exchange with lane^32 and one LDS exchange between the two vocabulary
 //     waves;
-//   * K is staged through LDS in 128-byte slabs (64 bf16 / 32 fp32) per row,
-//     double-buffered, with the 16-byte chunks of row r stored at chunk
-//     position (c ^ (r & 7)) so that the fragment reads of 8 consecutive
-//     lanes (8 different rows, same chunk) fall in 8 different bank groups;
+//   * K is staged through LDS in 128-byte slabs per row (whole cache lines),
+//     the 16-byte chunk c of row r stored at chunk slot c ^ f(r) with
+//     f(r) = (r & 7) ^ ((r >> 3) & 1): the fragment reads of 16 consecutive
+//     lanes (16 rows, one chunk) then hit 16 distinct bank groups;
 //   * workgroups are renumbered so that each XCD (private L2) walks a
-//     contiguous range of tiles, and inside it groups of kGroupV vocabulary
-//     stripes are swept across all position tiles, so a W stripe is fetched
-//     from HBM about once and re-read from L2 by the position tiles.
+//     contiguous range of tiles, sweeping groups of kGroupV vocabulary
+//     stripes across all position tiles, so concurrently running workgroups
+//     share W and hidden stripes in L2.
+//
+// bf16 path (the hot one): K is fed to LDS by buffer loads that write LDS
+// directly (no register staging).  W gets a 3-slot ring (prefetched two
+// stages ahead: it streams from HBM), hidden a 2-slot ring (one stage ahead:
+// it stays in the last-level cache): 5 x 32 KiB = the whole 160 KiB of LDS.
+// One barrier per 64-element K stage; inside a stage the fragment reads of
+// the next 16-element sub-step are interleaved with the current MFMAs.
+// fp32 path (small problems): register-staged double buffer.
 #include "fork_kernels.h"
 
 #include <math.h>
@@ -39,16 +47,21 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 512;
-constexpr int kSlabBytes = 128;                       // bytes of K per row per stage
-constexpr int kOperandBytes = kTileV * kSlabBytes;    // 32 KiB (kTileV == kTileP)
-constexpr int kGroupV = 4;                            // vocab stripes per sweep group
+constexpr int kSlab = 128;                   // bytes of K per row per stage
+constexpr int kOperandBytes = 256 * kSlab;   // 32 KiB: one operand, one stage
+constexpr int kGroupV = 8;                   // vocab stripes per sweep group
 constexpr int kXcds = 8;
 constexpr float kLog2e = 1.4426950408889634f;
+// Raw-buffer descriptor word 3 for gfx9-family buffers: 32-bit data format,
+// offsets checked against the record count (out of range reads return 0).
+constexpr int kBufferWord3 = 0x00020000;
+constexpr unsigned kOutOfRange = 0x80000000u;
 
-static_assert(kTileV == kTileP, "LDS layout assumes square tiles");
+static_assert(kTileV == 256 && kTileP == 256, "tile layout assumes 256 x 256");
 
-__device__ __forceinline__ int swz(int row, int chunk) {
-  return row * kSlabBytes + ((chunk ^ (row & 7)) << 4);
+__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+  return row * kSlab + ((chunk ^ swz(row)) << 4);
 }
 
 // Maps the hardware workgroup id to (vocabulary tile, position tile).
@@ -90,127 +103,13 @@ __device__ __forceinline__ int acc_row(int i, int e, int lane) {
   return i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
 }
 
-template <bool kBF16>
-__global__ __launch_bounds__(kThreads) void gemm_stats_kernel(
-    const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W,
-    int M, int d, int V, int nvt, int npt, float4* __restrict__ partials) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[4 * kOperandBytes];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wv = wave & 1;   // vocabulary half: rows wv*128 .. +128
-  const int wp = wave >> 1;  // position quarter: cols wp*64 .. +64
-
-  int vt, pt;
-  map_tile(blockIdx.x, nvt, npt, vt, pt);
-  const int v0 = vt * kTileV;
-  const int p0 = pt * kTileP;
-
-  const size_t row_bytes = (size_t)d * (kBF16 ? 2 : 4);
-  const int kchunks = (int)(row_bytes >> 4);       // 16-byte chunks per row
-  const int nk = (kchunks + 7) >> 3;               // 128-byte stages
-
-  // Global -> LDS copy assignment: thread owns chunk c of rows r0 + 64*i.
-  const int c = tid & 7;
-  const int r0 = tid >> 3;
-  const unsigned char* ga[4];
-  const unsigned char* gb[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    // Rows past the end re-read the last row; their results are discarded.
-    const int vr = min(v0 + r0 + 64 * i, V - 1);
-    const int pr = min(p0 + r0 + 64 * i, M - 1);
-    ga[i] = W + (size_t)vr * row_bytes + (c << 4);
-    gb[i] = hidden + (size_t)pr * row_bytes + (c << 4);
-  }
-  uint4 ra[4], rb[4];
-  auto gload = [&](int kt) {
-    const bool ok = (kt * 8 + c) < kchunks;  // chunks past d are zero on both sides
-    const size_t off = (size_t)kt * kSlabBytes;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = ok ? *reinterpret_cast<const uint4*>(ga[i] + off) : make_uint4(0, 0, 0, 0);
-      rb[i] = ok ? *reinterpret_cast<const uint4*>(gb[i] + off) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-    unsigned char* sa = smem + (buf * 2 + 0) * kOperandBytes;
-    unsigned char* sb = smem + (buf * 2 + 1) * kOperandBytes;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(sa + swz(r0 + 64 * i, c)) = ra[i];
-      *reinterpret_cast<uint4*>(sb + swz(r0 + 64 * i, c)) = rb[i];
-    }
-  };
-
-  f32x16 acc[4][2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int arow = wv * 128 + (lane & 31);  // + i*32
-  const int brow = wp * 64 + (lane & 31);   // + j*32
-  const int khalf = lane >> 5;
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const unsigned char* sa = smem + (buf * 2 + 0) * kOperandBytes;
-    const unsigned char* sb = smem + (buf * 2 + 1) * kOperandBytes;
-    if constexpr (kBF16) {
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {  // 16 bf16 of K per MFMA
-        const int chunk = kk * 2 + khalf;
-        bf16x8 a[4], b[2];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a[i] = *reinterpret_cast<const bf16x8*>(sa + swz(arow + i * 32, chunk));
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          b[j] = *reinterpret_cast<const bf16x8*>(sb + swz(brow + j * 32, chunk));
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
-    } else {
-#pragma unroll 2
-      for (int q = 0; q < 8; ++q) {  // 4 fp32 of K per chunk, two MFMAs of K=2
-        float4 a[4], b[2];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a[i] = *reinterpret_cast<const float4*>(sa + swz(arow + i * 32, q));
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          b[j] = *reinterpret_cast<const float4*>(sb + swz(brow + j * 32, q));
-        // lanes 0-31 supply K index 0 of each pair, lanes 32-63 index 1
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const float a0 = khalf ? a[i].y : a[i].x, b0 = khalf ? b[j].y : b[j].x;
-            const float a1 = khalf ? a[i].w : a[i].z, b1 = khalf ? b[j].w : b[j].z;
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[i][j], 0, 0, 0);
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[i][j], 0, 0, 0);
-          }
-      }
-    }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  // ---- epilogue: per-position statistics over this workgroup's 256 rows of W
-  float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP], LDS is free now
-  const int vbase = v0 + wv * 128;                 // first vocabulary row of the wave
+// Per-(position, tile) statistics from the accumulators of one wave, combined
+// across the two vocabulary waves through LDS, stored to partials.
+__device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned char* smem, int tid,
+                                         int lane, int wv, int wp, int vt, int v0, int p0, int M,
+                                         int V, float4* __restrict__ partials) {
+  float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
+  const int vbase = v0 + wv * 128;
   const bool full = v0 + kTileV <= V;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -254,32 +153,316 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_kernel(
     s += __shfl_xor(s, 32);
     t += __shfl_xor(t, 32);
     if (lane < 32)
-      red[wv * kTileP + wp * 64 + j * 32 + lane] =
-          make_float4(m, s, t, __int_as_float(idx));
+      red[wv * kTileP + wp * 64 + j * 32 + lane] = make_float4(m, s, t, __int_as_float(idx));
   }
   __syncthreads();
   if (tid < kTileP) {
     const int r = p0 + tid;
-    if (r < M) {
-      const float4 out = merge2(red[tid], red[kTileP + tid]);
-      partials[(size_t)vt * M + r] = out;
-    }
+    if (r < M) partials[(size_t)vt * M + r] = merge2(red[tid], red[kTileP + tid]);
   }
+}
+
+__device__ __forceinline__ void barrier_nofence() {
+  // s_barrier alone: the release fence of __syncthreads would also wait for
+  // the loads still in flight for later stages.  The empty asm statements
+  // keep the compiler from moving LDS accesses across the barrier.
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt with vmcnt <= n and lgkmcnt == 0 (expcnt not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+__global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
+    const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
+    int V, int nvt, int npt, float4* __restrict__ partials) {
+  // W ring: slots 0..2; hidden ring: slots 3..4
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[5 * kOperandBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wv = wave & 1;   // vocabulary half: rows wv*128 .. +128
+  const int wp = wave >> 1;  // position quarter: cols wp*64 .. +64
+
+  int vt, pt;
+  map_tile(blockIdx.x, nvt, npt, vt, pt);
+  const int v0 = vt * kTileV;
+  const int p0 = pt * kTileP;
+
+  const int row_bytes = d * 2;
+  const int kchunks = row_bytes >> 4;      // 16-byte chunks per row
+  const int nk = (kchunks + 7) >> 3;       // 128-byte stages
+
+  // Buffer descriptors rooted at this tile's first rows: rows past the end of
+  // W / hidden are outside the record count and read as zero.
+  const unsigned recW = (unsigned)(min(kTileV, V - v0) * row_bytes);
+  const unsigned recH = (unsigned)(min(kTileP, M - p0) * row_bytes);
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(W + (size_t)v0 * row_bytes), (short)0, (int)recW, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rsH = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(hidden + (size_t)p0 * row_bytes), (short)0, (int)recH, kBufferWord3);
+
+  // Each load instruction of a wave writes 1 KiB of LDS = 8 rows x 128 B;
+  // lane i fills chunk slot i % 8 of row drow + 8q, so it loads the logical
+  // chunk stored there.  Rows drow + 8q with odd q differ in bit 3, which
+  // flips bit 0 of the swizzle.
+  const int slot_in_row = lane & 7;
+  const int drow = wave * 32 + (lane >> 3);
+  const int dchunk0 = slot_in_row ^ swz(drow);
+  const int dchunk1 = dchunk0 ^ 1;
+  const unsigned off0 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk0 << 4);
+  const unsigned off1 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk1 << 4);
+  const unsigned qstride = (unsigned)(8 * row_bytes);
+  auto src_off = [&](int s, int q) -> unsigned {
+    const int c = (q & 1) ? dchunk1 : dchunk0;
+    const unsigned o = (q & 1) ? off1 : off0;
+    // chunks past d read as zero (the offset lies beyond every record count)
+    return (s * 8 + c < kchunks) ? o + (unsigned)(s * kSlab) + (unsigned)q * qstride : kOutOfRange;
+  };
+  auto issue_W = [&](int s, int slot) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsW, (__attribute__((address_space(3))) void*)(smem + slot * kOperandBytes + (wave * 4 + q) * 1024),
+          16, src_off(s, q), 0, 0, 0);
+  };
+  auto issue_H = [&](int s, int slot) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsH, (__attribute__((address_space(3))) void*)(smem + (3 + slot) * kOperandBytes + (wave * 4 + q) * 1024),
+          16, src_off(s, q), 0, 0, 0);
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // Fragment addressing: rows arow + 32i share the swizzle of arow.
+  const int arow = wv * 128 + (lane & 31);
+  const int brow = wp * 64 + (lane & 31);
+  const int khalf = lane >> 5;  // lanes 32..63 supply the upper 8 of 16 K values
+  const int fa = swz(arow), fb = swz(brow);
+
+  auto load_frags = [&](int ws, int hs, int kk, bf16x8 (&a)[4], bf16x8 (&b)[2]) {
+    const unsigned char* sa = smem + ws * kOperandBytes;
+    const unsigned char* sb = smem + (3 + hs) * kOperandBytes;
+    const int chunk = kk * 2 + khalf;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[i] = *reinterpret_cast<const bf16x8*>(sa + (arow + i * 32) * kSlab + ((chunk ^ fa) << 4));
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      b[j] = *reinterpret_cast<const bf16x8*>(sb + (brow + j * 32) * kSlab + ((chunk ^ fb) << 4));
+  };
+  // Eight MFMAs on (ac, bc) with the six reads of the next fragments (an, bn)
+  // interleaved; with `dma`, the loads of hidden stage s_dma - 1 and W stage
+  // s_dma are issued in the second half.
+  auto phase = [&](const bf16x8 (&ac)[4], const bf16x8 (&bc)[2], int ws, int hs, int kk,
+                   bf16x8 (&an)[4], bf16x8 (&bn)[2], bool dma, int s_dma, int ws_dma,
+                   int hs_dma) {
+    const unsigned char* sa = smem + ws * kOperandBytes;
+    const unsigned char* sb = smem + (3 + hs) * kOperandBytes;
+    const int chunk = kk * 2 + khalf;
+    const int ca = (chunk ^ fa) << 4, cb = (chunk ^ fb) << 4;
+    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[0], bc[0], acc[0][0], 0, 0, 0);
+    bn[0] = *reinterpret_cast<const bf16x8*>(sb + brow * kSlab + cb);
+    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[0], bc[1], acc[0][1], 0, 0, 0);
+    bn[1] = *reinterpret_cast<const bf16x8*>(sb + (brow + 32) * kSlab + cb);
+    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[1], bc[0], acc[1][0], 0, 0, 0);
+    an[0] = *reinterpret_cast<const bf16x8*>(sa + arow * kSlab + ca);
+    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[1], bc[1], acc[1][1], 0, 0, 0);
+    an[1] = *reinterpret_cast<const bf16x8*>(sa + (arow + 32) * kSlab + ca);
+    acc[2][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[0], acc[2][0], 0, 0, 0);
+    an[2] = *reinterpret_cast<const bf16x8*>(sa + (arow + 64) * kSlab + ca);
+    if (dma) issue_H(s_dma - 1, hs_dma);
+    acc[2][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[1], acc[2][1], 0, 0, 0);
+    an[3] = *reinterpret_cast<const bf16x8*>(sa + (arow + 96) * kSlab + ca);
+    acc[3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[0], acc[3][0], 0, 0, 0);
+    if (dma) issue_W(s_dma, ws_dma);
+    acc[3][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[1], acc[3][1], 0, 0, 0);
+    // schedule: (MFMA, read) x 5, loads, MFMA, read, MFMA, loads, MFMA
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  };
+
+  bf16x8 a0[4], b0[2], a1[4], b1[2];
+  // Prologue: hidden 0, W 0 and W 1 resident; hidden 1 and W 2 in flight.
+  // At the barrier of stage k the loop issues hidden k+2 then W k+3, so the
+  // newest loads at any barrier are W's.  Stages past the end read as zero
+  // into slots nobody reads again.
+  issue_H(0, 0);
+  issue_W(0, 0);
+  issue_W(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  barrier_nofence();
+  issue_H(1, 1);
+  issue_W(2, 2);
+  load_frags(0, 0, 0, a0, b0);
+  int ws = 0, hs = 0;
+  for (int k = 0; k + 1 < nk; ++k) {
+    const int ws1 = ws == 2 ? 0 : ws + 1, hs1 = hs ^ 1;
+    phase(a0, b0, ws, hs, 1, a1, b1, false, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    phase(a1, b1, ws, hs, 2, a0, b0, false, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    phase(a0, b0, ws, hs, 3, a1, b1, false, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // hidden k+1 and W k+1 landed (only W k+2, the last 4 loads, may still be
+    // in flight); every read of stage k has returned
+    wait_vm_lgkm0<4>();
+    barrier_nofence();
+    phase(a1, b1, ws1, hs1, 0, a0, b0, true, k + 3, ws, hs);
+    __builtin_amdgcn_sched_barrier(0);
+    ws = ws1;
+    hs = hs1;
+  }
+  phase(a0, b0, ws, hs, 1, a1, b1, false, 0, 0, 0);
+  phase(a1, b1, ws, hs, 2, a0, b0, false, 0, 0, 0);
+  phase(a0, b0, ws, hs, 3, a1, b1, false, 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  barrier_nofence();
+
+  epilogue(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials);
+}
+
+// fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
+// 16-byte chunk.
+__global__ __launch_bounds__(kThreads) void gemm_stats_f32_kernel(
+    const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
+    int V, int nvt, int npt, float4* __restrict__ partials) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[4 * kOperandBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wv = wave & 1;
+  const int wp = wave >> 1;
+
+  int vt, pt;
+  map_tile(blockIdx.x, nvt, npt, vt, pt);
+  const int v0 = vt * kTileV;
+  const int p0 = pt * kTileP;
+
+  const size_t row_bytes = (size_t)d * 4;
+  const int kchunks = (int)(row_bytes >> 4);
+  const int nk = (kchunks + 7) >> 3;
+
+  // Global -> LDS copy assignment: thread owns chunk c of rows r0 + 64*i.
+  const int c = tid & 7;
+  const int r0 = tid >> 3;
+  const unsigned char* ga[4];
+  const unsigned char* gb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // Rows past the end re-read the last row; their results are discarded.
+    const int vr = min(v0 + r0 + 64 * i, V - 1);
+    const int pr = min(p0 + r0 + 64 * i, M - 1);
+    ga[i] = W + (size_t)vr * row_bytes + (c << 4);
+    gb[i] = hidden + (size_t)pr * row_bytes + (c << 4);
+  }
+  uint4 ra[4], rb[4];
+  auto gload = [&](int kt) {
+    const bool ok = (kt * 8 + c) < kchunks;  // chunks past d are zero on both sides
+    const size_t off = (size_t)kt * kSlab;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = ok ? *reinterpret_cast<const uint4*>(ga[i] + off) : make_uint4(0, 0, 0, 0);
+      rb[i] = ok ? *reinterpret_cast<const uint4*>(gb[i] + off) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto sstore = [&](int buf) {
+    unsigned char* sa = smem + (buf * 2 + 0) * kOperandBytes;
+    unsigned char* sb = smem + (buf * 2 + 1) * kOperandBytes;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<uint4*>(sa + lds_off(r0 + 64 * i, c)) = ra[i];
+      *reinterpret_cast<uint4*>(sb + lds_off(r0 + 64 * i, c)) = rb[i];
+    }
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int arow = wv * 128 + (lane & 31);
+  const int brow = wp * 64 + (lane & 31);
+  const int khalf = lane >> 5;
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+    const unsigned char* sa = smem + (buf * 2 + 0) * kOperandBytes;
+    const unsigned char* sb = smem + (buf * 2 + 1) * kOperandBytes;
+#pragma unroll 2
+    for (int q = 0; q < 8; ++q) {  // 4 fp32 of K per chunk, two MFMAs of K=2
+      float4 a[4], b[2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const float4*>(sa + lds_off(arow + i * 32, q));
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = *reinterpret_cast<const float4*>(sb + lds_off(brow + j * 32, q));
+      // lanes 0-31 supply K index 0 of each pair, lanes 32-63 index 1
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const float a0 = khalf ? a[i].y : a[i].x, b0 = khalf ? b[j].y : b[j].x;
+          const float a1 = khalf ? a[i].w : a[i].z, b1 = khalf ? b[j].w : b[j].z;
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[i][j], 0, 0, 0);
+        }
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  epilogue(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials);
 }
 
 }  // namespace
 
-hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M,
-                             int d, int V, float4* partials, hipStream_t stream) {
+hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M, int d, int V,
+                             float4* partials, hipStream_t stream) {
   const int nvt = num_vocab_tiles(V);
   const int npt = num_pos_tiles(M);
   const dim3 grid((unsigned)(nvt * npt)), block(kThreads);
   if (bf16)
-    hipLaunchKernelGGL(gemm_stats_kernel<true>, grid, block, 0, stream,
+    hipLaunchKernelGGL(gemm_stats_bf16_kernel, grid, block, 0, stream,
                        static_cast<const unsigned char*>(hidden),
                        static_cast<const unsigned char*>(W), M, d, V, nvt, npt, partials);
   else
-    hipLaunchKernelGGL(gemm_stats_kernel<false>, grid, block, 0, stream,
+    hipLaunchKernelGGL(gemm_stats_f32_kernel, grid, block, 0, stream,
                        static_cast<const unsigned char*>(hidden),
                        static_cast<const unsigned char*>(W), M, d, V, nvt, npt, partials);
   return hipGetLastError();

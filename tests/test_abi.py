@@ -79,6 +79,7 @@ def _args(**kw):
     (dict(rule=5), _binding.FORK_EINVAL),
     (dict(d=12), _binding.FORK_EUNSUPPORTED),
     (dict(d=6, dtype=_binding.FORK_F32), _binding.FORK_EUNSUPPORTED),
+    (dict(d=(1 << 20) + 8), _binding.FORK_EUNSUPPORTED),
     (dict(hidden=18), _binding.FORK_EINVAL),
     (dict(B=1 << 16, L=1 << 16), _binding.FORK_EINVAL),
     (dict(workspace=256, workspace_bytes=10), _binding.FORK_EINVAL),
