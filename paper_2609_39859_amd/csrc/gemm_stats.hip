@@ -34,7 +34,9 @@
 // stages ahead: it streams from HBM), hidden a 2-slot ring (one stage ahead:
 // it stays in the last-level cache): 5 x 32 KiB = the whole 160 KiB of LDS.
 // One barrier per 64-element K stage; inside a stage the fragment reads of
-// the next 16-element sub-step are interleaved with the current MFMAs.
+// the next 16-element sub-step are interleaved with the current MFMAs, and
+// the buffer loads of later stages are spread over the stage in small groups
+// so that no wave stalls its MFMA stream behind a burst of loads.
 // fp32 path (small problems): register-staged double buffer.
 #include "fork_kernels.h"
 
@@ -219,18 +221,26 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
   const unsigned off0 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk0 << 4);
   const unsigned off1 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk1 << 4);
   const unsigned qstride = (unsigned)(8 * row_bytes);
-  auto src_off = [&](int s, int q) -> unsigned {
-    const int c = (q & 1) ? dchunk1 : dchunk0;
-    const unsigned o = (q & 1) ? off1 : off0;
-    // chunks past d read as zero (the offset lies beyond every record count)
-    return (s * 8 + c < kchunks) ? o + (unsigned)(s * kSlab) + (unsigned)q * qstride : kOutOfRange;
-  };
-  auto issue_W = [&](int s, int slot) {
+  unsigned qoff[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+  for (int q = 0; q < 4; ++q) qoff[q] = ((q & 1) ? off1 : off0) + (unsigned)q * qstride;
+  const int kfull = kchunks >> 3;  // stages whose chunks all lie inside d
+  auto src_off = [&](int s, int q) -> unsigned {
+    if (s < kfull) return qoff[q] + (unsigned)(s * kSlab);
+    // chunks past d read as zero (the offset lies beyond every record count)
+    const int c = (q & 1) ? dchunk1 : dchunk0;
+    return (s * 8 + c < kchunks) ? qoff[q] + (unsigned)(s * kSlab) : kOutOfRange;
+  };
+  auto issue_W2 = [&](int s, int slot, int q0) {  // sub-blocks q0, q0 + 1 of W stage s
+#pragma unroll
+    for (int q = q0; q < q0 + 2; ++q)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rsW, (__attribute__((address_space(3))) void*)(smem + slot * kOperandBytes + (wave * 4 + q) * 1024),
           16, src_off(s, q), 0, 0, 0);
+  };
+  auto issue_W = [&](int s, int slot) {
+    issue_W2(s, slot, 0);
+    issue_W2(s, slot, 2);
   };
   auto issue_H = [&](int s, int slot) {
 #pragma unroll
@@ -266,11 +276,11 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
       b[j] = *reinterpret_cast<const bf16x8*>(sb + (brow + j * 32) * kSlab + ((chunk ^ fb) << 4));
   };
   // Eight MFMAs on (ac, bc) with the six reads of the next fragments (an, bn)
-  // interleaved; with `dma`, the loads of hidden stage s_dma - 1 and W stage
-  // s_dma are issued in the second half.
+  // interleaved one per MFMA.  `mode` adds loads after the sixth MFMA:
+  // 1 = hidden stage s_dma (4 loads), 2 / 3 = W stage s_dma sub-blocks 0-1 /
+  // 2-3 (2 loads), each pair separated by an MFMA.
   auto phase = [&](const bf16x8 (&ac)[4], const bf16x8 (&bc)[2], int ws, int hs, int kk,
-                   bf16x8 (&an)[4], bf16x8 (&bn)[2], bool dma, int s_dma, int ws_dma,
-                   int hs_dma) {
+                   bf16x8 (&an)[4], bf16x8 (&bn)[2], int mode, int s_dma, int slot_dma) {
     const unsigned char* sa = smem + ws * kOperandBytes;
     const unsigned char* sb = smem + (3 + hs) * kOperandBytes;
     const int chunk = kk * 2 + khalf;
@@ -285,60 +295,67 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
     an[1] = *reinterpret_cast<const bf16x8*>(sa + (arow + 32) * kSlab + ca);
     acc[2][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[0], acc[2][0], 0, 0, 0);
     an[2] = *reinterpret_cast<const bf16x8*>(sa + (arow + 64) * kSlab + ca);
-    if (dma) issue_H(s_dma - 1, hs_dma);
     acc[2][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[1], acc[2][1], 0, 0, 0);
     an[3] = *reinterpret_cast<const bf16x8*>(sa + (arow + 96) * kSlab + ca);
+    if (mode == 1) issue_H(s_dma, slot_dma);
+    else if (mode == 2) issue_W2(s_dma, slot_dma, 0);
+    else if (mode == 3) issue_W2(s_dma, slot_dma, 2);
     acc[3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[0], acc[3][0], 0, 0, 0);
-    if (dma) issue_W(s_dma, ws_dma);
     acc[3][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[1], acc[3][1], 0, 0, 0);
-    // schedule: (MFMA, read) x 5, loads, MFMA, read, MFMA, loads, MFMA
 #pragma unroll
-    for (int q = 0; q < 5; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (mode == 1) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // buffer loads
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    } else if (mode >= 2) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    } else {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
   };
 
   bf16x8 a0[4], b0[2], a1[4], b1[2];
-  // Prologue: hidden 0, W 0 and W 1 resident; hidden 1 and W 2 in flight.
-  // At the barrier of stage k the loop issues hidden k+2 then W k+3, so the
-  // newest loads at any barrier are W's.  Stages past the end read as zero
-  // into slots nobody reads again.
+  // Load order: H0 W0 W1 H1, then per stage k: W(k+2) during the stage's
+  // first two sub-steps, H(k+2) right after the stage's barrier.  At the
+  // barrier of stage k only W(k+2), the 4 newest loads, may be in flight, and
+  // every slot refilled after it belongs to a stage all waves have finished
+  // reading.  Stages past the end read as zero into slots nobody reads again.
   issue_H(0, 0);
   issue_W(0, 0);
   issue_W(1, 1);
-  __builtin_amdgcn_s_waitcnt(0);
-  barrier_nofence();
   issue_H(1, 1);
-  issue_W(2, 2);
+  wait_vm_lgkm0<8>();  // H0 and W0 resident
+  barrier_nofence();
   load_frags(0, 0, 0, a0, b0);
-  int ws = 0, hs = 0;
+  int ws = 0, hs = 0, ws2 = 2;  // W slots of stages k and k + 2, hidden slot of k
   for (int k = 0; k + 1 < nk; ++k) {
     const int ws1 = ws == 2 ? 0 : ws + 1, hs1 = hs ^ 1;
-    phase(a0, b0, ws, hs, 1, a1, b1, false, 0, 0, 0);
+    phase(a0, b0, ws, hs, 1, a1, b1, 2, k + 2, ws2);
     __builtin_amdgcn_sched_barrier(0);
-    phase(a1, b1, ws, hs, 2, a0, b0, false, 0, 0, 0);
+    phase(a1, b1, ws, hs, 2, a0, b0, 3, k + 2, ws2);
     __builtin_amdgcn_sched_barrier(0);
-    phase(a0, b0, ws, hs, 3, a1, b1, false, 0, 0, 0);
+    phase(a0, b0, ws, hs, 3, a1, b1, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
-    // hidden k+1 and W k+1 landed (only W k+2, the last 4 loads, may still be
-    // in flight); every read of stage k has returned
+    // hidden and W of stage k+1 resident; all reads of stage k returned
     wait_vm_lgkm0<4>();
     barrier_nofence();
-    phase(a1, b1, ws1, hs1, 0, a0, b0, true, k + 3, ws, hs);
+    phase(a1, b1, ws1, hs1, 0, a0, b0, 1, k + 2, hs);
     __builtin_amdgcn_sched_barrier(0);
     ws = ws1;
     hs = hs1;
+    ws2 = ws2 == 2 ? 0 : ws2 + 1;
   }
-  phase(a0, b0, ws, hs, 1, a1, b1, false, 0, 0, 0);
-  phase(a1, b1, ws, hs, 2, a0, b0, false, 0, 0, 0);
-  phase(a0, b0, ws, hs, 3, a1, b1, false, 0, 0, 0);
+  phase(a0, b0, ws, hs, 1, a1, b1, 0, 0, 0);
+  phase(a1, b1, ws, hs, 2, a0, b0, 0, 0, 0);
+  phase(a0, b0, ws, hs, 3, a1, b1, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
