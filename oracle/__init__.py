@@ -13,7 +13,9 @@ Algorithm 2, Algorithm 1 for the differential tests, Section 3.2):
   (lowest index of the maximum logit), confidence q(candidate), log q of the
   candidate, log-normaliser, entropy in nats and the top-2 logit gap.
 * ``select`` -- the unmasking rule inside the active block (threshold set,
-  then leftmost or highest-confidence fallback), applied to copies.
+  then leftmost or highest-confidence fallback), applied to copies;
+  ``select_ex`` adds the fallback ablations of Section 4.1 (lowest
+  confidence, highest entropy, uniformly random masked position).
 * ``step`` -- both, over every row.
 """
 from __future__ import annotations
@@ -32,6 +34,9 @@ BF16 = 0
 F32 = 1
 RULE_LEFTMOST = 0
 RULE_MAXCONF = 1
+RULE_MINCONF = 2
+RULE_MAXENT = 3
+RULE_RANDOM = 4
 
 def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
     """Compile the oracle with gcc (plain C99 + OpenMP)."""
@@ -74,6 +79,11 @@ class Oracle:
         lib.oracle_select.argtypes = [ctypes.c_int32, ctypes.c_int32,
                                       ctypes.c_int32, P, P, ctypes.c_double,
                                       ctypes.c_int, P, P, P, P, P]
+        lib.oracle_select_ex.restype = ctypes.c_int
+        lib.oracle_select_ex.argtypes = [ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32, P, P, P, P,
+                                         ctypes.c_double, ctypes.c_int,
+                                         P, P, P, P, P]
         self.lib = lib
 
     def row_stats(self, hidden, W, rows=None, nthreads: int = 0):
@@ -127,6 +137,36 @@ class Oracle:
             raise ValueError("oracle_select rejected its arguments (%d)" % rc)
         return tok, msk, bs, fb, nc
 
+    def select_ex(self, conf, argmax_tok, tokens, mask, block_start, B, L,
+                  block_len, lam, rule=RULE_LEFTMOST, entropy=None, uniform=None):
+        """select() with every fallback rule, including the Section 4.1
+        ablations (entropy [B*L] for RULE_MAXENT, uniform [B] float32 in
+        [0, 1) for RULE_RANDOM)."""
+        conf = np.ascontiguousarray(conf, dtype=np.float64).reshape(-1)
+        argmax_tok = np.ascontiguousarray(argmax_tok, dtype=np.int32).reshape(-1)
+        tok = np.array(tokens, dtype=np.int32, copy=True).reshape(-1)
+        msk = np.array(mask, dtype=np.uint8, copy=True).reshape(-1)
+        bs = np.array(block_start, dtype=np.int32, copy=True).reshape(-1)
+        if conf.size != B * L or argmax_tok.size != B * L or tok.size != B * L \
+                or msk.size != B * L or bs.size != B:
+            raise ValueError("array sizes do not match B=%d, L=%d" % (B, L))
+        ent = None if entropy is None else np.ascontiguousarray(entropy, dtype=np.float64).reshape(-1)
+        uni = None if uniform is None else np.ascontiguousarray(uniform, dtype=np.float32).reshape(-1)
+        if ent is not None and ent.size != B * L:
+            raise ValueError("entropy must have B*L entries")
+        if uni is not None and uni.size != B:
+            raise ValueError("uniform must have B entries")
+        fb = np.empty(B, np.int32)
+        nc = np.empty(B, np.int32)
+        rc = self.lib.oracle_select_ex(B, L, block_len, _ptr(conf),
+                                       None if ent is None else _ptr(ent),
+                                       None if uni is None else _ptr(uni),
+                                       _ptr(argmax_tok), float(lam), int(rule),
+                                       _ptr(tok), _ptr(msk), _ptr(bs), _ptr(fb), _ptr(nc))
+        if rc != 0:
+            raise ValueError("oracle_select_ex rejected its arguments (%d)" % rc)
+        return tok, msk, bs, fb, nc
+
     def step(self, hidden, W, tokens, mask, block_start, B, L, block_len, lam,
              rule=RULE_LEFTMOST, nthreads: int = 0):
         """One full step on every row: statistics, then selection."""
@@ -153,6 +193,10 @@ def row_stats(*a, **k):
 
 def select(*a, **k):
     return default().select(*a, **k)
+
+
+def select_ex(*a, **k):
+    return default().select_ex(*a, **k)
 
 
 def step(*a, **k):

@@ -116,17 +116,53 @@ int oracle_row_stats(const void* hidden, const void* W, int dtype, int64_t d,
   return status;
 }
 
-/* Algorithm 2 (Fork-dLLM) and Algorithm 1 (Fast-dLLM) applied inside the
- * active block of the semi-autoregressive regime (Section 4.1, block length
- * BL); the fallback flag is membership of the step in F_i (Section 3.2). */
-int oracle_select(int32_t B, int32_t L, int32_t block_len, const double* conf,
-                  const int32_t* argmax_tok, double lambda, int rule,
-                  int32_t* tokens, uint8_t* mask, int32_t* block_start,
-                  int32_t* fallback, int32_t* ncommit) {
+/* The single position committed on a fallback step, among the masked
+ * positions of [s, e) of sequence row `base`. */
+static int32_t fallback_pick(int rule, const double* conf, const double* entropy,
+                             const float* uniform, int32_t b, int64_t base,
+                             const uint8_t* mask, int32_t s, int32_t e) {
+  int32_t pick = -1;
+  if (rule == ORACLE_RULE_RANDOM) {
+    int32_t n = 0;
+    for (int32_t k = s; k < e; ++k) n += mask[base + k] ? 1 : 0;
+    float prod = uniform[b] * (float)n;  /* binary32, as the method's draw */
+    int32_t j = (int32_t)prod;
+    if (j > n - 1) j = n - 1;
+    if (j < 0) j = 0;
+    for (int32_t k = s; k < e; ++k)
+      if (mask[base + k] && j-- == 0) return k;
+    return -1;
+  }
+  for (int32_t k = s; k < e; ++k) {
+    if (!mask[base + k]) continue;
+    if (pick < 0) {
+      pick = k;
+      if (rule == ORACLE_RULE_LEFTMOST) break;
+      continue;
+    }
+    const double* key = rule == ORACLE_RULE_MAXENT ? entropy : conf;
+    const double cand = key[base + k], best = key[base + pick];
+    const int better = rule == ORACLE_RULE_MINCONF ? (cand < best) : (cand > best);
+    if (better) pick = k;
+  }
+  return pick;
+}
+
+/* Algorithm 2 (Fork-dLLM), Algorithm 1 (Fast-dLLM) and the fallback
+ * ablations of Section 4.1, applied inside the active block of the
+ * semi-autoregressive regime (Section 4.1, block length BL); the fallback
+ * flag is membership of the step in F_i (Section 3.2). */
+int oracle_select_ex(int32_t B, int32_t L, int32_t block_len, const double* conf,
+                     const double* entropy, const float* uniform,
+                     const int32_t* argmax_tok, double lambda, int rule,
+                     int32_t* tokens, uint8_t* mask, int32_t* block_start,
+                     int32_t* fallback, int32_t* ncommit) {
   if (B <= 0 || L <= 0 || block_len <= 0 || !conf || !argmax_tok || !tokens ||
       !mask || !block_start || !fallback)
     return -1;
-  if (rule != ORACLE_RULE_LEFTMOST && rule != ORACLE_RULE_MAXCONF) return -1;
+  if (rule < ORACLE_RULE_LEFTMOST || rule > ORACLE_RULE_RANDOM) return -1;
+  if (rule == ORACLE_RULE_MAXENT && !entropy) return -1;
+  if (rule == ORACLE_RULE_RANDOM && !uniform) return -1;
   for (int32_t b = 0; b < B; ++b) {
     const int64_t base = (int64_t)b * L;
     if (block_start[b] < 0 || block_start[b] > L) return -1;
@@ -157,15 +193,10 @@ int oracle_select(int32_t B, int32_t L, int32_t block_len, const double* conf,
       }
     if (n == 0) {
       /* fallback: exactly one position */
-      int32_t pick = -1;
-      for (int32_t k = s; k < e; ++k) {
-        if (!mask[base + k]) continue;
-        if (pick < 0) {
-          pick = k;
-          if (rule == ORACLE_RULE_LEFTMOST) break;
-        } else if (conf[base + k] > conf[base + pick]) {
-          pick = k;
-        }
+      const int32_t pick = fallback_pick(rule, conf, entropy, uniform, b, base, mask, s, e);
+      if (pick < s || pick >= e) {
+        free(in_u);
+        return -1;
       }
       in_u[pick - s] = 1;
       n = 1;
@@ -183,4 +214,13 @@ int oracle_select(int32_t B, int32_t L, int32_t block_len, const double* conf,
     if (ncommit) ncommit[b] = n;
   }
   return 0;
+}
+
+int oracle_select(int32_t B, int32_t L, int32_t block_len, const double* conf,
+                  const int32_t* argmax_tok, double lambda, int rule,
+                  int32_t* tokens, uint8_t* mask, int32_t* block_start,
+                  int32_t* fallback, int32_t* ncommit) {
+  if (rule != ORACLE_RULE_LEFTMOST && rule != ORACLE_RULE_MAXCONF) return -1;
+  return oracle_select_ex(B, L, block_len, conf, NULL, NULL, argmax_tok, lambda,
+                          rule, tokens, mask, block_start, fallback, ncommit);
 }

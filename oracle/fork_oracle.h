@@ -25,8 +25,11 @@ extern "C" {
 #endif
 
 enum { ORACLE_BF16 = 0, ORACLE_F32 = 1 };
-enum { ORACLE_RULE_LEFTMOST = 0,   /* Fork-dLLM fallback (Algorithm 2)  */
-       ORACLE_RULE_MAXCONF = 1 };  /* Fast-dLLM fallback (Algorithm 1)  */
+enum { ORACLE_RULE_LEFTMOST = 0,   /* Fork-dLLM fallback (Algorithm 2)      */
+       ORACLE_RULE_MAXCONF = 1,    /* Fast-dLLM fallback (Algorithm 1)      */
+       ORACLE_RULE_MINCONF = 2,    /* ablations of Section 4.1: lowest      */
+       ORACLE_RULE_MAXENT = 3,     /*   confidence, highest entropy,        */
+       ORACLE_RULE_RANDOM = 4 };   /*   uniformly random masked position    */
 
 /*
  * Per-position statistics of the model distribution q^k(. | x_t) for the
@@ -73,6 +76,23 @@ int oracle_select(int32_t B, int32_t L, int32_t block_len,
                   double lambda, int rule,
                   int32_t* tokens, uint8_t* mask, int32_t* block_start,
                   int32_t* fallback, int32_t* ncommit);
+
+/*
+ * oracle_select with the fallback ablations of Section 4.1 as well:
+ *   MINCONF: the masked position of lowest confidence (lowest k on ties);
+ *   MAXENT:  the masked position of highest entropy (lowest k on ties);
+ *   RANDOM:  with n masked positions in the block and u = uniform[b] in
+ *            [0, 1), the j-th of them in increasing order, j = (int)(u * n)
+ *            evaluated in binary32 and capped at n - 1.
+ * entropy ([B*L]) is read by MAXENT only, uniform ([B]) by RANDOM only; either
+ * may be NULL when its rule is not used.
+ */
+int oracle_select_ex(int32_t B, int32_t L, int32_t block_len,
+                     const double* conf, const double* entropy,
+                     const float* uniform, const int32_t* argmax_tok,
+                     double lambda, int rule,
+                     int32_t* tokens, uint8_t* mask, int32_t* block_start,
+                     int32_t* fallback, int32_t* ncommit);
 
 #ifdef __cplusplus
 }

@@ -33,8 +33,12 @@ MUTATIONS = {
                            "if (rule == ORACLE_RULE_LEFTMOST) continue;"),
     "fallback_flag_swapped": ("fallback[b] = 1;\n    } else {\n      fallback[b] = 0;",
                               "fallback[b] = 0;\n    } else {\n      fallback[b] = 1;"),
-    "fast_tie_highest": ("} else if (conf[base + k] > conf[base + pick]) {",
-                         "} else if (conf[base + k] >= conf[base + pick]) {"),
+    "fast_tie_highest": ("(cand < best) : (cand > best);", "(cand <= best) : (cand >= best);"),
+    "minconf_as_maxconf": ("rule == ORACLE_RULE_MINCONF ? (cand < best)", "rule == ORACLE_RULE_MINCONF ? (cand > best)"),
+    "maxent_reads_conf": ("const double* key = rule == ORACLE_RULE_MAXENT ? entropy : conf;",
+                          "const double* key = conf;"),
+    "random_off_by_one": ("if (mask[base + k] && j-- == 0) return k;", "if (mask[base + k] && --j == 0) return k;"),
+    "random_rounds_up": ("int32_t j = (int32_t)prod;", "int32_t j = (int32_t)(prod + 0.5f);"),
     "no_skip_forward": ("s += block_len;", "break;"),
 }
 
@@ -55,6 +59,8 @@ def _checks(orc):
         lambda: pins.test_select_invariants(orc, 0, 0.8),
         lambda: pins.test_fork_vs_fast_differential(orc, 0),
         lambda: pins.test_fast_fallback_tie_takes_lowest_position(orc),
+        lambda: pins.test_fallback_ablations_hand_worked(orc),
+        lambda: pins.test_fallback_ablation_properties(orc, 0),
     ]
     failed = 0
     for c in calls:

@@ -340,3 +340,80 @@ def test_fast_fallback_tie_takes_lowest_position(orc):
     assert t.tolist() == [9, -1, 6, -1] and m.tolist() == [0, 1, 0, 1] and fb.tolist() == [1]
     t, m, _, fb, _ = orc.select(conf, am, tok, msk, bs, 1, 4, 3, 0.5, oracle.RULE_LEFTMOST)
     assert t.tolist() == [9, 5, -1, -1] and m.tolist() == [0, 0, 1, 1] and fb.tolist() == [1]
+
+
+RULES = {"LEFTMOST": oracle.RULE_LEFTMOST, "MAXCONF": oracle.RULE_MAXCONF,
+         "MINCONF": oracle.RULE_MINCONF, "MAXENT": oracle.RULE_MAXENT}
+
+
+def test_fallback_ablations_hand_worked(orc):
+    """Section 4.1's fallback ablations on a hand-worked block
+    (tests/golden/select_ablations.json)."""
+    with open(os.path.join(GOLDEN, "select_ablations.json")) as f:
+        g = json.load(f)
+    L, BL, lam = g["L"], g["block_len"], g["lambda"]
+    conf = np.array(g["conf"])
+    ent = np.array(g["entropy"])
+    msk = np.array(g["mask"], np.uint8)
+    tok = np.where(msk, -1, 4).astype(np.int32)
+    am = np.arange(L, dtype=np.int32) + 100
+    bs = np.array([1], np.int32)
+    for name, pos in g["expect"].items():
+        t, m, _, fb, nc = orc.select_ex(conf, am, tok, msk, bs, 1, L, BL, lam, RULES[name], entropy=ent)
+        assert fb.tolist() == [1] and nc.tolist() == [1], name
+        assert [k for k in range(L) if msk[k] and not m[k]] == [pos], name
+        assert t[pos] == 100 + pos
+    for u, pos in g["random"]:
+        _, m, _, fb, _ = orc.select_ex(conf, am, tok, msk, bs, 1, L, BL, lam, oracle.RULE_RANDOM,
+                                       uniform=np.array([u], np.float32))
+        assert [k for k in range(L) if msk[k] and not m[k]] == [pos], u
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_fallback_ablation_properties(orc, seed):
+    """On random blocks every rule commits one masked position of the
+    active block on a fallback step, with the property its name states; on
+    parallel steps all rules agree with Algorithm 2."""
+    rng = np.random.default_rng(500 + seed)
+    B, L, BL, lam = 6, 40, 8, 0.8
+    for _ in range(15):
+        msk = (rng.random(B * L) < 0.5).astype(np.uint8)
+        tok = np.where(msk, -1, 7).astype(np.int32)
+        bs = (rng.integers(0, 5, B) * BL).astype(np.int32)
+        conf = rng.random(B * L) * rng.choice([0.85, 1.0], B * L)
+        ent = rng.random(B * L) * 5
+        uni = rng.random(B).astype(np.float32)
+        am = rng.integers(0, 50, B * L).astype(np.int32)
+        ref = orc.select(conf, am, tok, msk, bs, B, L, BL, lam)
+        for rule in (oracle.RULE_MINCONF, oracle.RULE_MAXENT, oracle.RULE_RANDOM):
+            out = orc.select_ex(conf, am, tok, msk, bs, B, L, BL, lam, rule, entropy=ent, uniform=uni)
+            assert np.array_equal(out[2], ref[2]) and np.array_equal(out[3], ref[3])
+            for b in range(B):
+                sl = slice(b * L, (b + 1) * L)
+                if ref[3][b] != 1:
+                    assert np.array_equal(out[1][sl], ref[1][sl])
+                    continue
+                s = ref[2][b]
+                blk = [k for k in range(s, min(s + BL, L)) if msk[b * L + k]]
+                pick = [k for k in range(L) if msk[b * L + k] and not out[1][b * L + k]]
+                assert len(pick) == 1 and pick[0] in blk
+                key = {oracle.RULE_MINCONF: [-conf[b * L + k] for k in blk],
+                       oracle.RULE_MAXENT: [ent[b * L + k] for k in blk]}.get(rule)
+                if key is not None:
+                    assert pick[0] == blk[int(np.argmax(key))]
+                else:
+                    j = min(int(np.float32(uni[b]) * np.float32(len(blk))), len(blk) - 1)
+                    assert pick[0] == blk[j]
+
+
+def test_select_ex_rejects_missing_inputs(orc):
+    z = np.zeros(4)
+    a = np.zeros(4, np.int32)
+    m = np.ones(4, np.uint8)
+    bs = np.array([0], np.int32)
+    with pytest.raises(ValueError):
+        orc.select_ex(z, a, a, m, bs, 1, 4, 4, 0.5, oracle.RULE_MAXENT)
+    with pytest.raises(ValueError):
+        orc.select_ex(z, a, a, m, bs, 1, 4, 4, 0.5, oracle.RULE_RANDOM)
+    with pytest.raises(ValueError):
+        orc.select_ex(z, a, a, m, bs, 1, 4, 4, 0.5, 9)
