@@ -59,11 +59,17 @@ enum {
 /* Element types of hidden and W_head (both the same). */
 enum { FORK_BF16 = 0, FORK_F32 = 1 };
 
-/* Fallback rules when no masked position of the active block passes tau. */
+/* Fallback rules when no masked position of the active block passes tau.
+   Ties go to the lowest position. */
 enum {
   FORK_RULE_LEFTMOST = 0, /* Fork-dLLM, Algorithm 2: the leftmost masked position */
-  FORK_RULE_MAXCONF = 1   /* Fast-dLLM, Algorithm 1: the highest confidence
-                             (lowest position on ties)                          */
+  FORK_RULE_MAXCONF = 1,  /* Fast-dLLM, Algorithm 1: the highest confidence       */
+  FORK_RULE_MINCONF = 2,  /* ablations of Section 4.1: the lowest confidence,     */
+  FORK_RULE_MAXENT = 3,   /*   the highest entropy,                               */
+  FORK_RULE_RANDOM = 4    /*   or a uniformly random masked position: with n
+                               masked positions and u = fallback_uniform[b], the
+                               j-th in increasing order, j = (int)(u * n) in
+                               binary32, capped at n - 1                          */
 };
 
 /* Values written to out_fallback[b]. */
@@ -143,6 +149,9 @@ typedef struct fork_step_args {
      can time that kernel alone with hipEventElapsedTime. */
   void* ev_lmhead_begin;
   void* ev_lmhead_end;
+  /* [B] float in [0, 1): the random draw of each sequence for
+     FORK_RULE_RANDOM (required by that rule, ignored by the others). */
+  const float* fallback_uniform;
 } fork_step_args;
 
 /* fork_step with the extras above.  Same return codes. */

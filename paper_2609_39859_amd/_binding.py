@@ -25,6 +25,9 @@ FORK_BF16 = 0
 FORK_F32 = 1
 FORK_RULE_LEFTMOST = 0
 FORK_RULE_MAXCONF = 1
+FORK_RULE_MINCONF = 2
+FORK_RULE_MAXENT = 3
+FORK_RULE_RANDOM = 4
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -42,6 +45,7 @@ class ForkStepArgs(ctypes.Structure):
         ("out_commit_pos", _P), ("rule", _I32),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("ev_lmhead_begin", _P), ("ev_lmhead_end", _P),
+        ("fallback_uniform", _P),
     ]
 
 
@@ -124,7 +128,7 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
                  B: int, L: int, out_lse=None, out_argmax=None, out_ncommit=None,
                  out_commit_pos=None, rule: int = FORK_RULE_LEFTMOST,
                  workspace: Optional[torch.Tensor] = None, stream=None,
-                 events=None) -> None:
+                 events=None, fallback_uniform=None) -> None:
     """fork_step_ex of the C ABI; optional outputs may be None.  ``events``
     is an optional pair of raw hipEvent_t handles (ints) recorded around the
     LM-head kernel."""
@@ -170,6 +174,7 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
         a.workspace_bytes = workspace.numel() * workspace.element_size()
     if events is not None:
         a.ev_lmhead_begin, a.ev_lmhead_end = events
+    a.fallback_uniform = _opt(fallback_uniform, "fallback_uniform", torch.float32, B, device)
     rc = lib().fork_step_ex(ctypes.byref(a))
     if rc != FORK_OK:
         raise ForkError(rc, lib().fork_last_error().decode())

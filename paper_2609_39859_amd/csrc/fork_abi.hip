@@ -101,8 +101,10 @@ int validate(const fork_step_args* a) {
   if (!isfinite(a->tau)) return fail(FORK_EINVAL, "tau must be finite");
   if (a->dtype != FORK_BF16 && a->dtype != FORK_F32)
     return fail(FORK_EINVAL, "unknown dtype %d", a->dtype);
-  if (a->rule != FORK_RULE_LEFTMOST && a->rule != FORK_RULE_MAXCONF)
+  if (a->rule < FORK_RULE_LEFTMOST || a->rule > FORK_RULE_RANDOM)
     return fail(FORK_EINVAL, "unknown fallback rule %d", a->rule);
+  if (a->rule == FORK_RULE_RANDOM && !a->fallback_uniform)
+    return fail(FORK_EINVAL, "FORK_RULE_RANDOM needs fallback_uniform");
   if (a->dtype == FORK_BF16 && a->d % 8 != 0)
     return fail(FORK_EUNSUPPORTED, "bf16 path needs d %% 8 == 0 (d=%d)", a->d);
   if (a->dtype == FORK_F32 && a->d % 4 != 0)
@@ -154,9 +156,10 @@ int fork_step_ex(const fork_step_args* a) {
   e = fork::launch_merge(partials, M, nvt, a->out_conf, a->out_entropy, a->out_logp, a->out_lse,
                          argmax, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
-  e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf, argmax,
-                          a->tokens, a->mask, a->block_start, a->out_fallback, a->out_ncommit,
-                          a->out_commit_pos, stream);
+  e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf,
+                          a->out_entropy, a->fallback_uniform, argmax, a->tokens, a->mask,
+                          a->block_start, a->out_fallback, a->out_ncommit, a->out_commit_pos,
+                          stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "select launch: %s", hipGetErrorString(e));
 
   static const bool sync_each = [] {

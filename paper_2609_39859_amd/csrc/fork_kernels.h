@@ -36,9 +36,11 @@ hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse,
                         int32_t* argmax, hipStream_t stream);
 
-// Unmasking rule per sequence, in place.  ncommit / commit_pos may be null.
+// Unmasking rule per sequence, in place.  ncommit / commit_pos may be null;
+// entropy is read by the highest-entropy rule, uniform by the random rule.
 hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
-                         const float* conf, const int32_t* argmax,
+                         const float* conf, const float* entropy, const float* uniform,
+                         const int32_t* argmax,
                          int32_t* tokens, uint8_t* mask, int32_t* block_start,
                          int32_t* fallback, int32_t* ncommit,
                          int32_t* commit_pos, hipStream_t stream);

@@ -15,7 +15,9 @@
 // semi-autoregressive regime of Section 4.1): one wave64 per sequence; the
 // threshold test is a ballot over the block's lanes, the fallback is the
 // first set bit of the mask ballot (leftmost masked position), and committed
-// positions are compacted with a lane-prefix count.
+// positions are compacted with a lane-prefix count.  The other fallback rules
+// (Algorithm 1's highest confidence; Section 4.1's ablations: lowest
+// confidence, highest entropy, random position) are wave reductions.
 #include "fork_kernels.h"
 
 #include <math.h>
@@ -70,8 +72,12 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
 
 __device__ __forceinline__ unsigned long long ballot(bool p) { return __ballot(p); }
 
+// rule values as in the C ABI
+enum { kLeftmost = 0, kMaxConf = 1, kMinConf = 2, kMaxEnt = 3, kRandom = 4 };
+
 __global__ __launch_bounds__(64) void select_kernel(
     int L, int BL, float tau, int rule, const float* __restrict__ conf,
+    const float* __restrict__ entropy, const float* __restrict__ uniform,
     const int32_t* __restrict__ argmax, int32_t* __restrict__ tokens,
     uint8_t* __restrict__ mask, int32_t* __restrict__ block_start,
     int32_t* __restrict__ fallback, int32_t* __restrict__ ncommit,
@@ -123,7 +129,7 @@ __global__ __launch_bounds__(64) void select_kernel(
   const bool fb = npass == 0;
   int pick = -1;
   if (fb) {
-    if (rule == 0) {
+    if (rule == kLeftmost) {
       // leftmost masked position of the block
       for (int c = s; c < e; c += 64) {
         const int k = c + lane;
@@ -133,15 +139,37 @@ __global__ __launch_bounds__(64) void select_kernel(
           break;
         }
       }
+    } else if (rule == kRandom) {
+      // the j-th masked position, j = (int)(u * n) in binary32, capped
+      int n = 0;
+      for (int c = s; c < e; c += 64) n += __popcll(ballot(c + lane < e && mask[base + c + lane] != 0));
+      int j = (int)(uniform[b] * (float)n);
+      j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
+      for (int c = s; c < e; c += 64) {
+        const int k = c + lane;
+        const bool masked = k < e && mask[base + k] != 0;
+        const unsigned long long bm = ballot(masked);
+        const int cnt = __popcll(bm);
+        if (j < cnt) {
+          const int below = __popcll(bm & ((1ull << lane) - 1ull));
+          const unsigned long long hit = ballot(masked && below == j);
+          pick = c + __ffsll((long long)hit) - 1;
+          break;
+        }
+        j -= cnt;
+      }
     } else {
-      // highest confidence, lowest position on ties
-      float best = -INFINITY;
+      // extreme of confidence (highest or lowest) or of entropy (highest),
+      // lowest position on ties
+      const float* key = rule == kMaxEnt ? entropy : conf;
+      const bool lowest = rule == kMinConf;
+      float best = 0.f;
       int bi = 0x7fffffff;
       for (int c = s; c < e; c += 64) {
         const int k = c + lane;
         if (k < e && mask[base + k] != 0) {
-          const float v = conf[base + k];
-          if (bi == 0x7fffffff || v > best) {
+          const float v = key[base + k];
+          if (bi == 0x7fffffff || (lowest ? v < best : v > best)) {
             best = v;
             bi = k;
           }
@@ -151,7 +179,8 @@ __global__ __launch_bounds__(64) void select_kernel(
       for (int off = 32; off > 0; off >>= 1) {
         const float ob = __shfl_xor(best, off);
         const int oi = __shfl_xor(bi, off);
-        if (oi != 0x7fffffff && (bi == 0x7fffffff || ob > best || (ob == best && oi < bi))) {
+        const bool better = lowest ? ob < best : ob > best;
+        if (oi != 0x7fffffff && (bi == 0x7fffffff || better || (ob == best && oi < bi))) {
           best = ob;
           bi = oi;
         }
@@ -198,12 +227,13 @@ hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
 }
 
 hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
-                         const float* conf, const int32_t* argmax, int32_t* tokens,
-                         uint8_t* mask, int32_t* block_start, int32_t* fallback,
-                         int32_t* ncommit, int32_t* commit_pos, hipStream_t stream) {
+                         const float* conf, const float* entropy, const float* uniform,
+                         const int32_t* argmax, int32_t* tokens, uint8_t* mask,
+                         int32_t* block_start, int32_t* fallback, int32_t* ncommit,
+                         int32_t* commit_pos, hipStream_t stream) {
   hipLaunchKernelGGL(select_kernel, dim3((unsigned)B), dim3(64), 0, stream, L,
-                     block_len, tau, rule, conf, argmax, tokens, mask, block_start,
-                     fallback, ncommit, commit_pos);
+                     block_len, tau, rule, conf, entropy, uniform, argmax, tokens, mask,
+                     block_start, fallback, ncommit, commit_pos);
   return hipGetLastError();
 }
 

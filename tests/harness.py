@@ -52,7 +52,7 @@ class GpuOut:
 
 
 def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
-             rule=_binding.FORK_RULE_LEFTMOST, workspace=None) -> GpuOut:
+             rule=_binding.FORK_RULE_LEFTMOST, workspace=None, uniform=None) -> GpuOut:
     """One step through fork_step_ex on the device of h_dev; host inputs for
     the state, host copies of every output."""
     dev = h_dev.device
@@ -67,9 +67,11 @@ def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
     fb = torch.full((B,), -9, **i32)
     nc = torch.full((B,), -9, **i32)
     cp = torch.full((B * block_len,), -9, **i32)
+    uni = None if uniform is None else torch.as_tensor(np.asarray(uniform, np.float32)).to(dev)
     _binding.fork_step_ex(h_dev, W_dev, tok, msk, bs, block_len, tau, conf, ent, logp, fb,
                           B=B, L=L, out_lse=lse, out_argmax=am, out_ncommit=nc,
-                          out_commit_pos=cp, rule=rule, workspace=workspace)
+                          out_commit_pos=cp, rule=rule, workspace=workspace,
+                          fallback_uniform=uni)
     torch.cuda.synchronize(dev)
     c = lambda t: t.cpu().numpy()
     return GpuOut(c(conf), c(ent), c(logp), c(lse), c(am), c(tok), c(msk), c(bs), c(fb),
@@ -122,7 +124,8 @@ def compare_stats(g: GpuOut, ref: dict, rows, hbits, Wbits, d: int, rep: Report)
     return rows[mism]
 
 
-def check_rule_on_own_stats(g: GpuOut, tokens, mask, block_start, B, L, BL, tau, rule, seqs):
+def check_rule_on_own_stats(g: GpuOut, tokens, mask, block_start, B, L, BL, tau, rule, seqs,
+                            uniform=None):
     """Property check, for decisions that sit on the threshold: the GPU's
     commits are exactly what the rule gives on the GPU's own binary32
     confidences (committed set inside the active block; all masked positions
@@ -150,20 +153,33 @@ def check_rule_on_own_stats(g: GpuOut, tokens, mask, block_start, B, L, BL, tau,
             assert g.fallback[b] == 1 and len(committed) == 1
             if rule == _binding.FORK_RULE_LEFTMOST:
                 assert committed == [blk[0]]
+            elif rule == _binding.FORK_RULE_RANDOM:
+                j = min(int(np.float32(uniform[b]) * np.float32(len(blk))), len(blk) - 1)
+                assert committed == [blk[j]]
             else:
-                best = max(g.conf[base + k] for k in blk)
-                assert committed == [min(k for k in blk if g.conf[base + k] == best)]
+                key = {_binding.FORK_RULE_MAXCONF: g.conf, _binding.FORK_RULE_MINCONF: -g.conf,
+                       _binding.FORK_RULE_MAXENT: g.entropy}[rule]
+                best = max(key[base + k] for k in blk)
+                assert committed == [min(k for k in blk if key[base + k] == best)]
         assert g.ncommit[b] == len(committed)
 
 
+# Fallback keys closer than this (oracle values) may be ordered either way by
+# the GPU's binary32 statistics: the lowest-confidence / highest-entropy pick
+# is then excluded from the exact comparison (and checked on the GPU's own
+# statistics instead).
+KEY_TIE_TOL = {2: 1e-5, 3: 1e-4}
+
+
 def compare_decisions(g: GpuOut, sel, conf_ref, tokens, mask, block_start, B, L, BL,
-                      tau, rep: Report, seqs=None, rule=0, near_tie_rows=()):
-    """sel = oracle.select output on oracle confidences and candidates."""
+                      tau, rep: Report, seqs=None, rule=0, near_tie_rows=(),
+                      entropy_ref=None, uniform=None):
+    """sel = oracle select output on oracle confidences and candidates."""
     tok_o, msk_o, bs_o, fb_o, nc_o = sel
     lam = float(np.float32(tau))
     seqs = list(range(B) if seqs is None else seqs)
     # GPU decisions always agree with the rule on its own statistics
-    check_rule_on_own_stats(g, tokens, mask, block_start, B, L, BL, tau, rule, seqs)
+    check_rule_on_own_stats(g, tokens, mask, block_start, B, L, BL, tau, rule, seqs, uniform)
     tie = set(int(r) for r in near_tie_rows)
     for b in seqs:
         sl = slice(b * L, (b + 1) * L)
@@ -174,6 +190,12 @@ def compare_decisions(g: GpuOut, sel, conf_ref, tokens, mask, block_start, B, L,
             e = min(s + BL, L)
             blk = [k for k in range(s, e) if mask[b * L + k]]
             near = any(abs(conf_ref[b * L + k] - lam) < THRESH_TOL for k in blk)
+            if fb_o[b] == 1 and rule in KEY_TIE_TOL and len(blk) > 1:
+                key = np.array([conf_ref[b * L + k] if rule == 2 else entropy_ref[b * L + k]
+                                for k in blk])
+                srt = np.sort(key)
+                gap = srt[1] - srt[0] if rule == 2 else srt[-1] - srt[-2]
+                near = near or gap < KEY_TIE_TOL[rule]
         if near:
             rep.near_threshold_seqs += 1
             continue

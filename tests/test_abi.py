@@ -77,6 +77,8 @@ def _args(**kw):
     (dict(tau=float("inf")), _binding.FORK_EINVAL),
     (dict(dtype=7), _binding.FORK_EINVAL),
     (dict(rule=5), _binding.FORK_EINVAL),
+    (dict(rule=-1), _binding.FORK_EINVAL),
+    (dict(rule=4), _binding.FORK_EINVAL),          # random rule without uniforms
     (dict(d=12), _binding.FORK_EUNSUPPORTED),
     (dict(d=6, dtype=_binding.FORK_F32), _binding.FORK_EUNSUPPORTED),
     (dict(d=(1 << 20) + 8), _binding.FORK_EUNSUPPORTED),

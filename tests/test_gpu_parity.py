@@ -39,7 +39,9 @@ def _say(*a):
 
 def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None):
     """Decode cfg in lock-step; rows_fn(step, mask, block_start) picks the rows
-    the oracle evaluates (default: all).  Returns the report."""
+    the oracle evaluates (default: all).  The random fallback rule draws one
+    uniform per sequence and step from a seeded generator.  Returns the
+    report and the number of steps."""
     W = synth.weights(cfg)
     Wd = W.to(DEV)
     Wb = host_bits(W)
@@ -52,15 +54,19 @@ def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None):
         hb = host_bits(h)
         rows = np.arange(cfg.M) if rows_fn is None else rows_fn(t, msk, bs)
         ref = oracle.row_stats(hb, Wb, rows)
-        g = gpu_step(h.to(DEV), Wd, tok, msk, bs, B, L, BL, cfg.tau, rule=rule)
+        uni = np.random.default_rng(cfg.seed + 7000 + t).random(B).astype(np.float32)
+        g = gpu_step(h.to(DEV), Wd, tok, msk, bs, B, L, BL, cfg.tau, rule=rule, uniform=uni)
         ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
         conf_full = np.full(cfg.M, np.nan)
+        ent_full = np.full(cfg.M, np.nan)
         am_full = np.zeros(cfg.M, np.int32)
         conf_full[rows] = ref["conf"]
+        ent_full[rows] = ref["entropy"]
         am_full[rows] = ref["argmax"]
-        sel = oracle.select(conf_full, am_full, tok, msk, bs, B, L, BL, _lam(cfg.tau), rule)
+        sel = oracle.select_ex(conf_full, am_full, tok, msk, bs, B, L, BL, _lam(cfg.tau), rule,
+                               entropy=ent_full, uniform=uni)
         compare_decisions(g, sel, conf_full, tok, msk, bs, B, L, BL, cfg.tau, rep,
-                          rule=rule, near_tie_rows=ties)
+                          rule=rule, near_tie_rows=ties, entropy_ref=ent_full, uniform=uni)
         tok, msk, bs = sel[0], sel[1], sel[2]
         t += 1
         assert t <= cfg.G + 1
@@ -184,6 +190,20 @@ def test_mid_planted_lockstep_decode(rule):
     assert steps < 0.9 * 39  # parallel steps happen
 
 
+@pytest.mark.parametrize("rule", [_binding.FORK_RULE_MINCONF, _binding.FORK_RULE_MAXENT,
+                                  _binding.FORK_RULE_RANDOM])
+@pytest.mark.parametrize("name", ["tiny_peaked", "mid_planted"])
+def test_fallback_ablations_lockstep(name, rule):
+    """The fallback ablations of Section 4.1 (lowest confidence, highest
+    entropy, random masked position) in lock-step with the oracle."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    rows_fn = None if name.startswith("tiny") else (lambda t, m, b: _active_rows(cfg, m, b))
+    rep, steps = lockstep_decode(cfg, rule=rule, rows_fn=rows_fn)
+    assert steps <= cfg.G
+    assert rep.near_threshold_seqs <= max(2, rep.seqs // 10)
+
+
 RAGGED = [
     # B, L, d, V, dtype, block_len
     (3, 37, 200, 1013, torch.bfloat16, 8),
@@ -196,7 +216,7 @@ RAGGED = [
 
 
 @pytest.mark.parametrize("B,L,d,V,dtype,BL", RAGGED)
-@pytest.mark.parametrize("rule", [0, 1])
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
 def test_ragged_shapes_and_random_states(B, L, d, V, dtype, BL, rule):
     """Shapes that are not multiples of the tiles, random masks and block
     starts (including idle sequences and block_start = L)."""
@@ -213,13 +233,15 @@ def test_ragged_shapes_and_random_states(B, L, d, V, dtype, BL, rule):
         msk[(B - 1) * L:] = 0  # an idle sequence
     hb, Wb = host_bits(h), host_bits(W)
     ref = oracle.row_stats(hb, Wb)
+    uni = rng.random(B).astype(np.float32)
     for tau in (0.05, 0.3):
-        g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, B, L, BL, tau, rule=rule)
+        g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, B, L, BL, tau, rule=rule, uniform=uni)
         rep = Report()
         ties = compare_stats(g, ref, np.arange(M), hb, Wb, d, rep)
-        sel = oracle.select(ref["conf"], ref["argmax"], tok, msk, bs, B, L, BL, _lam(tau), rule)
+        sel = oracle.select_ex(ref["conf"], ref["argmax"], tok, msk, bs, B, L, BL, _lam(tau), rule,
+                               entropy=ref["entropy"], uniform=uni)
         compare_decisions(g, sel, ref["conf"], tok, msk, bs, B, L, BL, tau, rep, rule=rule,
-                          near_tie_rows=ties)
+                          near_tie_rows=ties, entropy_ref=ref["entropy"], uniform=uni)
 
 
 def test_caller_workspace_and_determinism():
