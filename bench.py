@@ -12,7 +12,9 @@ second (B*L rows through the LM head) is reported beside it.  `roofline`
 covers the dominant kernel (the LM-head GEMM + statistics), timed with HIP
 events recorded around that kernel alone on the stream it runs on.
 `cpu_baseline` times the binary64 CPU oracle on a bounded sample of rows of
-the same workload and scales it to steps per second.
+the same workload and scales it to steps per second.  `active_rows_mode`
+times the same decode with the LM head restricted to each sequence's active
+block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload.
 """
 import argparse
 import ctypes
@@ -52,9 +54,9 @@ def _source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def _traffic_per_launch():
-    """HBM bytes per LM-head launch from the committed rocprofv3 counter runs,
-    if they were taken on the current kernel source; else None."""
+def _traffic_per_launch(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -62,7 +64,7 @@ def _traffic_per_launch():
         return None
     if t.get("kernel_source_sha256_16") != _source_hash():
         return None
-    return t.get("hbm_bytes_per_launch")
+    return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(cfg, W_dev, h_dev, target_s):
@@ -101,6 +103,8 @@ def main():
     ap.add_argument("--config", default="llada8b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-active-rows", action="store_true",
+                    help="skip the extra timing of the active-block-only LM head")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -145,52 +149,60 @@ def main():
     fb = torch.empty(B, dtype=torch.int32, device=dev)
 
     hip = _hip()
-    n_ev = args.steps
-    evs = []
-    for _ in range(2 * n_ev):
-        e = ctypes.c_void_p()
-        assert hip.hipEventCreate(ctypes.byref(e)) == 0
-        evs.append(e.value)
 
-    def step(i, events=None):
-        _binding.fork_step_ex(hs[i % n_batches], W, tok, msk, bs, BL, cfg.tau, conf, ent, logp,
-                              fb, B=B, L=L, events=events)
+    def reset():
+        # restart the decode so every timed step has masked positions to select
+        tok.copy_(tok0.to(dev))
+        msk.copy_(msk0.to(dev))
+        bs.copy_(bs0.to(dev))
+        torch.cuda.synchronize()
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    # restart the decode so every timed step has masked positions to select
-    tok.copy_(tok0.to(dev))
-    msk.copy_(msk0.to(dev))
-    bs.copy_(bs0.to(dev))
-    torch.cuda.synchronize()
+    def timed(rows_mode, steps, warmup):
+        """Warm up, restart the decode, then time `steps` steps: total time
+        from torch events on the current stream, LM-head time per step from
+        HIP events the library records around that kernel on the same
+        stream."""
+        evs = []
+        for _ in range(2 * steps):
+            e = ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(e)) == 0
+            evs.append(e.value)
+
+        def step(i, events=None):
+            _binding.fork_step_ex(hs[i % n_batches], W, tok, msk, bs, BL, cfg.tau, conf, ent,
+                                  logp, fb, B=B, L=L, events=events, rows_mode=rows_mode)
+
+        for i in range(warmup):
+            step(i)
+        torch.cuda.synchronize()
+        reset()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        start.record()
+        for i in range(steps):
+            step(i, (evs[2 * i], evs[2 * i + 1]))
+        stop.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        lm = []
+        for i in range(steps):
+            ms = ctypes.c_float()
+            assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
+            lm.append(ms.value)
+        for e in evs:
+            hip.hipEventDestroy(e)
+        return start.elapsed_time(stop), lm, wall
+
     print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
-
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record()
-    for i in range(args.steps):
-        step(i, (evs[2 * i], evs[2 * i + 1]))
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = start.elapsed_time(stop)
-    lm_ms = []
-    for i in range(n_ev):
-        ms = ctypes.c_float()
-        assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
-        lm_ms.append(ms.value)
-    for e in evs:
-        hip.hipEventDestroy(e)
+    total_ms, lm_ms, wall = timed(_binding.FORK_ROWS_ALL, args.steps, args.warmup)
 
     ms_per_step = total_ms / args.steps
     steps_per_s = 1000.0 / ms_per_step
     lm_avg_ms = sum(lm_ms) / len(lm_ms)
     flops = 2.0 * M * d * V
     achieved_tflops = flops / (lm_avg_ms * 1e-3) / 1e12
-    traffic = _traffic_per_launch()
+    traffic = _traffic_per_launch("gemm_stats_bf16_kernel")
 
     out = {
         "metric": METRIC,
@@ -219,6 +231,29 @@ def main():
                      "algorithmic_flops_per_launch": flops},
         "cpu_baseline": None,
     }
+    if not args.no_active_rows:
+        # The same workload with the LM head restricted to each sequence's
+        # active block (B*block_len rows): W is read once per step and the
+        # per-row work is small, so this mode is bounded by HBM bandwidth.
+        print("bench: timing %d steps, active-block rows only" % args.steps, file=sys.stderr,
+              flush=True)
+        a_total, a_lm, _ = timed(_binding.FORK_ROWS_ACTIVE, args.steps, args.warmup)
+        reset()
+        Ma = B * BL
+        a_ms = a_total / args.steps
+        a_lm_ms = sum(a_lm) / len(a_lm)
+        a_bytes = (V * d + Ma * d) * 2 + math.ceil(V / 256) * Ma * 16  # W, rows, partials
+        a_gbs = a_bytes / (a_lm_ms * 1e-3) / 1e9
+        out["active_rows_mode"] = {
+            "rows_per_step": Ma, "ms_per_step": a_ms, "steps_per_s": 1000.0 / a_ms,
+            "lmhead_ms": a_lm_ms,
+            "roofline": {"bound": "hbm", "achieved": a_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": a_gbs / PEAK_HBM_GBS,
+                         "traffic": _traffic_per_launch("gemm_stats_bf16_rows_kernel"),
+                         "kernel": "gemm_stats_bf16_rows_kernel (LM head on the active rows)",
+                         "algorithmic_bytes_per_launch": a_bytes,
+                         "mfma_frac": 2.0 * Ma * d * V / (a_lm_ms * 1e-3) / 1e12
+                                      / PEAK_BF16_TFLOPS}}
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)

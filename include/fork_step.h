@@ -72,6 +72,17 @@ enum {
                                binary32, capped at n - 1                          */
 };
 
+/* Which positions get statistics (fork_step_args.rows_mode). */
+enum {
+  FORK_ROWS_ALL = 0,    /* every one of the B*L positions                      */
+  FORK_ROWS_ACTIVE = 1  /* only the positions of each sequence's active block:
+                           the selection reads nothing else, so the decisions
+                           are those of FORK_ROWS_ALL; out_conf, out_entropy,
+                           out_logp, out_lse and out_argmax are written at
+                           those positions only and left untouched elsewhere.
+                           Needs B*L*d*element_size < 2^31.                    */
+};
+
 /* Values written to out_fallback[b]. */
 enum {
   FORK_STEP_PARALLEL = 0, /* at least one position passed tau, all committed   */
@@ -152,13 +163,15 @@ typedef struct fork_step_args {
   /* [B] float in [0, 1): the random draw of each sequence for
      FORK_RULE_RANDOM (required by that rule, ignored by the others). */
   const float* fallback_uniform;
+  int32_t rows_mode;       /* FORK_ROWS_*; fork_step uses FORK_ROWS_ALL        */
 } fork_step_args;
 
 /* fork_step with the extras above.  Same return codes. */
 int fork_step_ex(const fork_step_args* args);
 
 /* Device workspace bytes a step with these sizes needs (per-tile partial
-   statistics and the per-position candidates); 0 if the sizes are invalid. */
+   statistics, the per-position candidates and the active-row list); 0 if the
+   sizes are invalid. */
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
 
 /* Description of the last non-OK return on the calling thread ("" if none).

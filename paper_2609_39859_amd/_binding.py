@@ -28,6 +28,8 @@ FORK_RULE_MAXCONF = 1
 FORK_RULE_MINCONF = 2
 FORK_RULE_MAXENT = 3
 FORK_RULE_RANDOM = 4
+FORK_ROWS_ALL = 0
+FORK_ROWS_ACTIVE = 1
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -45,7 +47,7 @@ class ForkStepArgs(ctypes.Structure):
         ("out_commit_pos", _P), ("rule", _I32),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("ev_lmhead_begin", _P), ("ev_lmhead_end", _P),
-        ("fallback_uniform", _P),
+        ("fallback_uniform", _P), ("rows_mode", _I32),
     ]
 
 
@@ -128,7 +130,7 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
                  B: int, L: int, out_lse=None, out_argmax=None, out_ncommit=None,
                  out_commit_pos=None, rule: int = FORK_RULE_LEFTMOST,
                  workspace: Optional[torch.Tensor] = None, stream=None,
-                 events=None, fallback_uniform=None) -> None:
+                 events=None, fallback_uniform=None, rows_mode: int = FORK_ROWS_ALL) -> None:
     """fork_step_ex of the C ABI; optional outputs may be None.  ``events``
     is an optional pair of raw hipEvent_t handles (ints) recorded around the
     LM-head kernel."""
@@ -175,6 +177,7 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
     if events is not None:
         a.ev_lmhead_begin, a.ev_lmhead_end = events
     a.fallback_uniform = _opt(fallback_uniform, "fallback_uniform", torch.float32, B, device)
+    a.rows_mode = int(rows_mode)
     rc = lib().fork_step_ex(ctypes.byref(a))
     if rc != FORK_OK:
         raise ForkError(rc, lib().fork_last_error().decode())

@@ -35,9 +35,9 @@ int fail(int code, const char* fmt, ...) {
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Workspace layout: [partials: nvt*M float4][argmax: M int32].
+// Workspace layout: [partials: nvt*M float4][argmax: M int32][rows: M int32].
 struct Layout {
-  size_t partial_off, argmax_off, total;
+  size_t partial_off, argmax_off, rows_off, total;
 };
 
 bool layout_for(int32_t B, int32_t L, int32_t V, Layout* out) {
@@ -47,7 +47,8 @@ bool layout_for(int32_t B, int32_t L, int32_t V, Layout* out) {
   const size_t nvt = (size_t)fork::num_vocab_tiles(V);
   out->partial_off = 0;
   out->argmax_off = align_up(nvt * (size_t)M * sizeof(float4));
-  out->total = out->argmax_off + align_up((size_t)M * sizeof(int32_t));
+  out->rows_off = out->argmax_off + align_up((size_t)M * sizeof(int32_t));
+  out->total = out->rows_off + align_up((size_t)M * sizeof(int32_t));
   return true;
 }
 
@@ -113,6 +114,11 @@ int validate(const fork_step_args* a) {
     return fail(FORK_EUNSUPPORTED, "d=%d exceeds the supported maximum %d", a->d, kMaxD);
   if (!aligned16(a->hidden) || !aligned16(a->W_head))
     return fail(FORK_EINVAL, "hidden and W_head must be 16-byte aligned");
+  if (a->rows_mode != FORK_ROWS_ALL && a->rows_mode != FORK_ROWS_ACTIVE)
+    return fail(FORK_EINVAL, "unknown rows_mode %d", a->rows_mode);
+  if (a->rows_mode == FORK_ROWS_ACTIVE &&
+      (long long)a->B * a->L * a->d * (a->dtype == FORK_BF16 ? 2 : 4) >= (1LL << 31))
+    return fail(FORK_EUNSUPPORTED, "FORK_ROWS_ACTIVE needs B*L*d*element_size < 2^31");
   return FORK_OK;
 }
 
@@ -134,27 +140,36 @@ int fork_step_ex(const fork_step_args* a) {
     rc = get_workspace(lay.total, &ws);
     if (rc != FORK_OK) return rc;
   }
-  const int M = a->B * a->L;
+  const int Mh = a->B * a->L;                       // rows of hidden
+  const bool active = a->rows_mode == FORK_ROWS_ACTIVE;
+  const int M = active ? a->B * a->block_len : Mh;  // positions through the LM head
   const int nvt = fork::num_vocab_tiles(a->V);
   float4* partials = reinterpret_cast<float4*>(static_cast<char*>(ws) + lay.partial_off);
   int32_t* argmax = a->out_argmax ? a->out_argmax
                                   : reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.argmax_off);
+  int32_t* rowlist = active ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.rows_off)
+                            : nullptr;
   hipStream_t stream = static_cast<hipStream_t>(a->stream);
 
   hipError_t e;
+  if (active) {
+    e = fork::launch_active_rows(a->B, a->L, a->block_len, a->mask, a->block_start, rowlist,
+                                 stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "active_rows launch: %s", hipGetErrorString(e));
+  }
   if (a->ev_lmhead_begin) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_begin), stream);
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_gemm_stats(a->hidden, a->W_head, a->dtype == FORK_BF16, M, a->d, a->V,
-                              partials, stream);
+                              partials, rowlist, Mh, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "gemm_stats launch: %s", hipGetErrorString(e));
   if (a->ev_lmhead_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_end), stream);
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_merge(partials, M, nvt, a->out_conf, a->out_entropy, a->out_logp, a->out_lse,
-                         argmax, stream);
+                         argmax, rowlist, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
   e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf,
                           a->out_entropy, a->fallback_uniform, argmax, a->tokens, a->mask,

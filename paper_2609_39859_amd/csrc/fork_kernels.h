@@ -24,17 +24,26 @@ struct Partial {
 inline int num_vocab_tiles(int V) { return (V + kTileV - 1) / kTileV; }
 inline int num_pos_tiles(int M) { return (M + kTileP - 1) / kTileP; }
 
-// Logits of rows [0, M) of hidden against W (never stored) reduced to one
-// Partial per (vocabulary tile, position): partials[vt * M + r].
+// Logits of M positions against W (never stored) reduced to one Partial per
+// (vocabulary tile, position): partials[vt * M + p].  Position p is hidden row
+// p, or with a row list hidden row rowlist[p] (-1 = none) out of Mh rows.
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16,
                              int M, int d, int V, float4* partials,
-                             hipStream_t stream);
+                             const int32_t* rowlist, int Mh, hipStream_t stream);
 
 // Merge the partials of each position over all vocabulary tiles into the
-// per-position results.  lse may be null.
+// per-position results (position p lands in row p, or rowlist[p] if a row
+// list is given; -1 = dropped).  lse may be null.
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse,
-                        int32_t* argmax, hipStream_t stream);
+                        int32_t* argmax, const int32_t* rowlist, hipStream_t stream);
+
+// Rows of each sequence's active block (the same skip-forward as the
+// selection): rowlist[b * block_len + i] = b * L + s_b + i, -1 past the block
+// end or for sequences with nothing to commit.
+hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
+                              const int32_t* block_start, int32_t* rowlist,
+                              hipStream_t stream);
 
 // Unmasking rule per sequence, in place.  ncommit / commit_pos may be null;
 // entropy is read by the highest-entropy rule, uniform by the random rule.

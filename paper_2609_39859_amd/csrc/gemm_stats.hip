@@ -180,9 +180,10 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-__global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
+__device__ __forceinline__ void gemm_stats_bf16_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
-    int V, int nvt, int npt, float4* __restrict__ partials) {
+    int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
+    int Mh) {
   // W ring: slots 0..2; hidden ring: slots 3..4
   __shared__ __attribute__((aligned(1024))) unsigned char smem[5 * kOperandBytes];
 
@@ -204,11 +205,15 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
   // Buffer descriptors rooted at this tile's first rows: rows past the end of
   // W / hidden are outside the record count and read as zero.
   const unsigned recW = (unsigned)(min(kTileV, V - v0) * row_bytes);
-  const unsigned recH = (unsigned)(min(kTileP, M - p0) * row_bytes);
+  // With a row list, position p of the tile is hidden row rowlist[p0 + p]
+  // (-1: no row, reads as zero) and the descriptor spans all Mh rows.
+  const unsigned recH = rowlist ? (unsigned)(Mh * row_bytes)
+                                : (unsigned)(min(kTileP, M - p0) * row_bytes);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(W + (size_t)v0 * row_bytes), (short)0, (int)recW, kBufferWord3);
   const __amdgpu_buffer_rsrc_t rsH = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(hidden + (size_t)p0 * row_bytes), (short)0, (int)recH, kBufferWord3);
+      (void*)(hidden + (rowlist ? (size_t)0 : (size_t)p0 * row_bytes)), (short)0, (int)recH,
+      kBufferWord3);
 
   // Each load instruction of a wave writes 1 KiB of LDS = 8 rows x 128 B;
   // lane i fills chunk slot i % 8 of row drow + 8q, so it loads the logical
@@ -221,22 +226,31 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
   const unsigned off0 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk0 << 4);
   const unsigned off1 = (unsigned)(drow * row_bytes) + (unsigned)(dchunk1 << 4);
   const unsigned qstride = (unsigned)(8 * row_bytes);
-  unsigned qoff[4];
+  unsigned qoff[4], hoff[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) qoff[q] = ((q & 1) ? off1 : off0) + (unsigned)q * qstride;
+  for (int q = 0; q < 4; ++q) {
+    qoff[q] = ((q & 1) ? off1 : off0) + (unsigned)q * qstride;
+    hoff[q] = qoff[q];
+    if (rowlist) {
+      const int p = p0 + drow + 8 * q;
+      const int r = p < M ? rowlist[p] : -1;
+      hoff[q] = r >= 0 ? (unsigned)(r * row_bytes) + (unsigned)(((q & 1) ? dchunk1 : dchunk0) << 4)
+                       : kOutOfRange;
+    }
+  }
   const int kfull = kchunks >> 3;  // stages whose chunks all lie inside d
-  auto src_off = [&](int s, int q) -> unsigned {
-    if (s < kfull) return qoff[q] + (unsigned)(s * kSlab);
+  auto src_off = [&](const unsigned (&base)[4], int s, int q) -> unsigned {
+    if (s < kfull) return base[q] + (unsigned)(s * kSlab);
     // chunks past d read as zero (the offset lies beyond every record count)
     const int c = (q & 1) ? dchunk1 : dchunk0;
-    return (s * 8 + c < kchunks) ? qoff[q] + (unsigned)(s * kSlab) : kOutOfRange;
+    return (s * 8 + c < kchunks) ? base[q] + (unsigned)(s * kSlab) : kOutOfRange;
   };
   auto issue_W2 = [&](int s, int slot, int q0) {  // sub-blocks q0, q0 + 1 of W stage s
 #pragma unroll
     for (int q = q0; q < q0 + 2; ++q)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rsW, (__attribute__((address_space(3))) void*)(smem + slot * kOperandBytes + (wave * 4 + q) * 1024),
-          16, src_off(s, q), 0, 0, 0);
+          16, src_off(qoff, s, q), 0, 0, 0);
   };
   auto issue_W = [&](int s, int slot) {
     issue_W2(s, slot, 0);
@@ -247,7 +261,7 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
     for (int q = 0; q < 4; ++q)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rsH, (__attribute__((address_space(3))) void*)(smem + (3 + slot) * kOperandBytes + (wave * 4 + q) * 1024),
-          16, src_off(s, q), 0, 0, 0);
+          16, src_off(hoff, s, q), 0, 0, 0);
   };
 
   f32x16 acc[4][2];
@@ -369,9 +383,10 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_bf16_kernel(
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
 // 16-byte chunk.
-__global__ __launch_bounds__(kThreads) void gemm_stats_f32_kernel(
+__device__ __forceinline__ void gemm_stats_f32_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
-    int V, int nvt, int npt, float4* __restrict__ partials) {
+    int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
+    int Mh) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * kOperandBytes];
 
   const int tid = threadIdx.x;
@@ -398,7 +413,8 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_f32_kernel(
   for (int i = 0; i < 4; ++i) {
     // Rows past the end re-read the last row; their results are discarded.
     const int vr = min(v0 + r0 + 64 * i, V - 1);
-    const int pr = min(p0 + r0 + 64 * i, M - 1);
+    int pr = min(p0 + r0 + 64 * i, M - 1);
+    if (rowlist) pr = max(rowlist[pr], 0);  // positions without a row: any valid row
     ga[i] = W + (size_t)vr * row_bytes + (c << 4);
     gb[i] = hidden + (size_t)pr * row_bytes + (c << 4);
   }
@@ -467,21 +483,50 @@ __global__ __launch_bounds__(kThreads) void gemm_stats_f32_kernel(
   epilogue(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials);
 }
 
+// Entry points: positions = hidden rows 0..M-1, or gathered through a row
+// list (the active-block rows).  Separate symbols keep the row-list
+// branches out of the dense kernel and the two apart in kernel traces.
+#define FORK_GEMM_ENTRIES(T)                                                                   \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_kernel(                        \
+      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
+      int d, int V, int nvt, int npt, float4* __restrict__ partials) {                         \
+    gemm_stats_##T##_body(hidden, W, M, d, V, nvt, npt, partials, nullptr, M);                 \
+  }                                                                                            \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_kernel(                   \
+      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
+      int d, int V, int nvt, int npt, float4* __restrict__ partials,                           \
+      const int32_t* __restrict__ rowlist, int Mh) {                                           \
+    gemm_stats_##T##_body(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh);                \
+  }
+FORK_GEMM_ENTRIES(bf16)
+FORK_GEMM_ENTRIES(f32)
+#undef FORK_GEMM_ENTRIES
+
 }  // namespace
 
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M, int d, int V,
-                             float4* partials, hipStream_t stream) {
+                             float4* partials, const int32_t* rowlist, int Mh,
+                             hipStream_t stream) {
   const int nvt = num_vocab_tiles(V);
   const int npt = num_pos_tiles(M);
   const dim3 grid((unsigned)(nvt * npt)), block(kThreads);
-  if (bf16)
-    hipLaunchKernelGGL(gemm_stats_bf16_kernel, grid, block, 0, stream,
-                       static_cast<const unsigned char*>(hidden),
-                       static_cast<const unsigned char*>(W), M, d, V, nvt, npt, partials);
-  else
-    hipLaunchKernelGGL(gemm_stats_f32_kernel, grid, block, 0, stream,
-                       static_cast<const unsigned char*>(hidden),
-                       static_cast<const unsigned char*>(W), M, d, V, nvt, npt, partials);
+  const auto* h = static_cast<const unsigned char*>(hidden);
+  const auto* w = static_cast<const unsigned char*>(W);
+  if (rowlist) {
+    if (bf16)
+      hipLaunchKernelGGL(gemm_stats_bf16_rows_kernel, grid, block, 0, stream, h, w, M, d, V, nvt,
+                         npt, partials, rowlist, Mh);
+    else
+      hipLaunchKernelGGL(gemm_stats_f32_rows_kernel, grid, block, 0, stream, h, w, M, d, V, nvt,
+                         npt, partials, rowlist, Mh);
+  } else {
+    if (bf16)
+      hipLaunchKernelGGL(gemm_stats_bf16_kernel, grid, block, 0, stream, h, w, M, d, V, nvt, npt,
+                         partials);
+    else
+      hipLaunchKernelGGL(gemm_stats_f32_kernel, grid, block, 0, stream, h, w, M, d, V, nvt, npt,
+                         partials);
+  }
   return hipGetLastError();
 }
 

@@ -47,7 +47,7 @@ __device__ __forceinline__ float4 merge2(float4 a, float4 b) {
 __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
     const float4* __restrict__ partials, int M, int nvt, float* __restrict__ conf,
     float* __restrict__ entropy, float* __restrict__ logp, float* __restrict__ lse,
-    int32_t* __restrict__ argmax) {
+    int32_t* __restrict__ argmax, const int32_t* __restrict__ rowlist) {
   __shared__ float4 red[kMergeWaves][kMergeRows];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -58,15 +58,16 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
       acc = merge2(acc, partials[(size_t)j * M + r]);
   red[w][lane] = acc;
   __syncthreads();
-  if (w == 0 && r < M) {
+  const int dst = r < M ? (rowlist ? rowlist[r] : r) : -1;
+  if (w == 0 && dst >= 0) {
 #pragma unroll
     for (int k = 1; k < kMergeWaves; ++k) acc = merge2(acc, red[k][lane]);
     const float log_s = logf(acc.y);
-    conf[r] = 1.0f / acc.y;
-    logp[r] = -log_s;
-    entropy[r] = log_s - acc.z / acc.y;
-    if (lse) lse[r] = acc.x + log_s;
-    argmax[r] = __float_as_int(acc.w);
+    conf[dst] = 1.0f / acc.y;
+    logp[dst] = -log_s;
+    entropy[dst] = log_s - acc.z / acc.y;
+    if (lse) lse[dst] = acc.x + log_s;
+    argmax[dst] = __float_as_int(acc.w);
   }
 }
 
@@ -214,15 +215,53 @@ __global__ __launch_bounds__(64) void select_kernel(
   }
 }
 
+// Active block of each sequence (first block from block_start holding a
+// masked position, as in the selection) expanded to its rows.
+__global__ __launch_bounds__(64) void active_rows_kernel(int L, int BL,
+                                                        const uint8_t* __restrict__ mask,
+                                                        const int32_t* __restrict__ block_start,
+                                                        int32_t* __restrict__ rowlist) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const size_t base = (size_t)b * L;
+  int s = block_start[b];
+  bool found = false;
+  if (s >= 0 && s <= L) {
+    while (s < L) {
+      const int e = min(s + BL, L);
+      for (int c = s; c < e; c += 64) {
+        const int k = c + lane;
+        if (ballot(k < e && mask[base + k] != 0)) {
+          found = true;
+          break;
+        }
+      }
+      if (found) break;
+      s += BL;
+    }
+  }
+  const int e = found ? min(s + BL, L) : 0;
+  for (int i = lane; i < BL; i += 64)
+    rowlist[(size_t)b * BL + i] = (found && s + i < e) ? (int32_t)(base + s + i) : -1;
+}
+
 }  // namespace
+
+hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
+                              const int32_t* block_start, int32_t* rowlist,
+                              hipStream_t stream) {
+  hipLaunchKernelGGL(active_rows_kernel, dim3((unsigned)B), dim3(64), 0, stream, L, block_len,
+                     mask, block_start, rowlist);
+  return hipGetLastError();
+}
 
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse, int32_t* argmax,
-                        hipStream_t stream) {
+                        const int32_t* rowlist, hipStream_t stream) {
   const dim3 grid((unsigned)((M + kMergeRows - 1) / kMergeRows));
   const dim3 block(kMergeRows * kMergeWaves);
   hipLaunchKernelGGL(merge_kernel, grid, block, 0, stream, partials, M, nvt, conf,
-                     entropy, logp, lse, argmax);
+                     entropy, logp, lse, argmax, rowlist);
   return hipGetLastError();
 }
 

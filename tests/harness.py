@@ -52,9 +52,12 @@ class GpuOut:
 
 
 def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
-             rule=_binding.FORK_RULE_LEFTMOST, workspace=None, uniform=None) -> GpuOut:
+             rule=_binding.FORK_RULE_LEFTMOST, workspace=None, uniform=None,
+             rows_mode=_binding.FORK_ROWS_ALL) -> GpuOut:
     """One step through fork_step_ex on the device of h_dev; host inputs for
-    the state, host copies of every output."""
+    the state, host copies of every output.  Per-position outputs start as
+    NaN (statistics) and -7 (candidates), so rows a step leaves untouched are
+    visible."""
     dev = h_dev.device
     M = B * L
     tok = torch.as_tensor(np.asarray(tokens, np.int32)).to(dev)
@@ -71,7 +74,7 @@ def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
     _binding.fork_step_ex(h_dev, W_dev, tok, msk, bs, block_len, tau, conf, ent, logp, fb,
                           B=B, L=L, out_lse=lse, out_argmax=am, out_ncommit=nc,
                           out_commit_pos=cp, rule=rule, workspace=workspace,
-                          fallback_uniform=uni)
+                          fallback_uniform=uni, rows_mode=rows_mode)
     torch.cuda.synchronize(dev)
     c = lambda t: t.cpu().numpy()
     return GpuOut(c(conf), c(ent), c(logp), c(lse), c(am), c(tok), c(msk), c(bs), c(fb),

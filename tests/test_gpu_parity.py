@@ -8,6 +8,7 @@ times, on sampled rows the oracle evaluates one by one, plus properties that
 hold for every row.
 """
 import math
+import types
 
 import numpy as np
 import pytest
@@ -37,11 +38,13 @@ def _say(*a):
     print(*a, flush=True)
 
 
-def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None):
+def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None,
+                    rows_mode=_binding.FORK_ROWS_ALL):
     """Decode cfg in lock-step; rows_fn(step, mask, block_start) picks the rows
     the oracle evaluates (default: all).  The random fallback rule draws one
-    uniform per sequence and step from a seeded generator.  Returns the
-    report and the number of steps."""
+    uniform per sequence and step from a seeded generator.  With
+    FORK_ROWS_ACTIVE the rows outside the active blocks must come back
+    untouched.  Returns the report and the number of steps."""
     W = synth.weights(cfg)
     Wd = W.to(DEV)
     Wb = host_bits(W)
@@ -55,7 +58,10 @@ def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None):
         rows = np.arange(cfg.M) if rows_fn is None else rows_fn(t, msk, bs)
         ref = oracle.row_stats(hb, Wb, rows)
         uni = np.random.default_rng(cfg.seed + 7000 + t).random(B).astype(np.float32)
-        g = gpu_step(h.to(DEV), Wd, tok, msk, bs, B, L, BL, cfg.tau, rule=rule, uniform=uni)
+        g = gpu_step(h.to(DEV), Wd, tok, msk, bs, B, L, BL, cfg.tau, rule=rule, uniform=uni,
+                     rows_mode=rows_mode)
+        if rows_mode == _binding.FORK_ROWS_ACTIVE:
+            _check_untouched(g, _active_rows(cfg, msk, bs), cfg.M)
         ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
         conf_full = np.full(cfg.M, np.nan)
         ent_full = np.full(cfg.M, np.nan)
@@ -84,6 +90,24 @@ def _active_rows(cfg, msk, bs):
             s = int(bs[b]) + ((masked[0] - int(bs[b])) // cfg.block_len) * cfg.block_len
             rows += [b * cfg.L + k for k in range(s, min(s + cfg.block_len, cfg.L))]
     return np.array(sorted(set(rows)), np.int64)
+
+
+def _check_untouched(g, active, M):
+    """Rows outside the active blocks keep the harness's sentinels."""
+    other = np.setdiff1d(np.arange(M), active)
+    for k in ("conf", "entropy", "logp", "lse"):
+        assert np.all(np.isnan(getattr(g, k)[other])), k
+    assert np.all(g.argmax[other] == -7)
+
+
+def _same_on_active(a, b, active):
+    """Two steps agree bit for bit on the active rows and in every decision."""
+    for k in ("conf", "entropy", "logp", "lse"):
+        x, y = getattr(a, k)[active], getattr(b, k)[active]
+        assert np.array_equal(x.view(np.int32), y.view(np.int32)), k
+    assert np.array_equal(a.argmax[active], b.argmax[active])
+    for k in ("tokens", "mask", "block_start", "fallback", "ncommit", "commit_pos"):
+        assert np.array_equal(getattr(a, k), getattr(b, k)), k
 
 
 # ------------------------------------------------------------ small workloads
@@ -244,6 +268,48 @@ def test_ragged_shapes_and_random_states(B, L, d, V, dtype, BL, rule):
                           near_tie_rows=ties, entropy_ref=ref["entropy"], uniform=uni)
 
 
+@pytest.mark.parametrize("B,L,d,V,dtype,BL", RAGGED)
+@pytest.mark.parametrize("rule", [0, 3, 4])
+def test_active_rows_mode_matches_all_rows(B, L, d, V, dtype, BL, rule):
+    """FORK_ROWS_ACTIVE runs the LM head on the active blocks only: on those
+    rows every statistic is bit-identical to the all-rows step (each logit
+    accumulates the same products in the same order), the decisions are the
+    same, and every other row is left untouched."""
+    _need_gpu()
+    gen = torch.Generator().manual_seed(7 * B + L + d + V + rule)
+    M = B * L
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(dtype).to(DEV)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(dtype).to(DEV)
+    rng = np.random.default_rng(M + V + 1)
+    msk = (rng.random(M) < 0.5).astype(np.uint8)
+    tok = np.where(msk, -1, rng.integers(0, V, M)).astype(np.int32)
+    bs = rng.integers(0, L + 1, B).astype(np.int32)
+    if B > 1:
+        msk[(B - 1) * L:] = 0  # an idle sequence
+    uni = rng.random(B).astype(np.float32)
+    active = _active_rows(types.SimpleNamespace(B=B, L=L, block_len=BL), msk, bs)
+    for tau in (0.05, 0.3):
+        a = gpu_step(h, W, tok, msk, bs, B, L, BL, tau, rule=rule, uniform=uni)
+        b = gpu_step(h, W, tok, msk, bs, B, L, BL, tau, rule=rule, uniform=uni,
+                     rows_mode=_binding.FORK_ROWS_ACTIVE)
+        _same_on_active(a, b, active)
+        _check_untouched(b, active, M)
+
+
+@pytest.mark.parametrize("name,rule", [("tiny_peaked", 0), ("mid_planted", 0),
+                                       ("mid_planted", 1)])
+def test_active_rows_mode_lockstep_decode(name, rule):
+    """A whole decode in FORK_ROWS_ACTIVE against the oracle on the active
+    rows, in lock-step."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    rep, steps = lockstep_decode(cfg, rule=rule,
+                                 rows_fn=lambda t, m, b: _active_rows(cfg, m, b),
+                                 rows_mode=_binding.FORK_ROWS_ACTIVE)
+    assert steps <= cfg.G
+    assert rep.near_threshold_seqs <= max(2, rep.seqs // 10)
+
+
 def test_caller_workspace_and_determinism():
     """Caller-provided workspace gives the same bits as the library one, and
     repeated runs are bit-identical (fixed merge order, no atomics)."""
@@ -335,6 +401,32 @@ def test_full_size_step_sampled(name):
     assert np.all(g.commit_pos[:, 0] == cfg.P) and np.all(g.commit_pos[:, 1:] == -1)
     _say("full-size %s: %d rows ok (%d near-tie), max err %s" % (
         name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+
+
+@pytest.mark.parametrize("name", ["llada8b", "rollout"])
+def test_full_size_active_rows_mode(name):
+    """FORK_ROWS_ACTIVE at full size: bit-identical to the all-rows step on
+    the active rows, same decisions, other rows untouched; the active rows of
+    the first sequences against the oracle."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    W = synth.weights(cfg, device=DEV)
+    h = synth.hidden(cfg, 5, device=DEV)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    _say("full-size active %s: GPU steps" % name)
+    a = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    b = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
+                 rows_mode=_binding.FORK_ROWS_ACTIVE)
+    active = _active_rows(cfg, msk, bs)
+    assert active.size == cfg.B * cfg.block_len
+    _same_on_active(a, b, active)
+    _check_untouched(b, active, cfg.M)
+    rows = active[: 2 * cfg.block_len]
+    ref = oracle.row_stats(host_bits(h), host_bits(W), rows)
+    rep = Report()
+    compare_stats(b, ref, rows, host_bits(h), host_bits(W), cfg.d, rep)
+    _say("full-size active %s: ok, max err %s" % (
+        name, {k: "%.2e" % v for k, v in rep.max_err.items()}))
 
 
 @pytest.mark.parametrize("name", ["llada8b"])
