@@ -17,6 +17,10 @@ Algorithm 2, Algorithm 1 for the differential tests, Section 3.2):
   ``select_ex`` adds the fallback ablations of Section 4.1 (lowest
   confidence, highest entropy, uniformly random masked position).
 * ``step`` -- both, over every row.
+* ``row_sample`` -- sampled candidates at a temperature tau > 0 (the draw
+  x_0^k ~ q(. | x_t; tau) of Section 2, by the Gumbel-max property with
+  Philox4x32-10 draws), with the untempered q and log q of the drawn token;
+  ``philox``, ``exp_draw`` expose the generator.
 """
 from __future__ import annotations
 
@@ -84,7 +88,60 @@ class Oracle:
                                          ctypes.c_int32, P, P, P, P,
                                          ctypes.c_double, ctypes.c_int,
                                          P, P, P, P, P]
+        lib.oracle_philox4x32_10.restype = None
+        lib.oracle_philox4x32_10.argtypes = [P, P, P]
+        lib.oracle_exp_draw.restype = ctypes.c_double
+        lib.oracle_exp_draw.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
+                                        ctypes.c_int64, P]
+        lib.oracle_row_sample.restype = ctypes.c_int
+        lib.oracle_row_sample.argtypes = [P, P, ctypes.c_int, ctypes.c_int64,
+                                          ctypes.c_int64, P, ctypes.c_int64,
+                                          ctypes.c_double, ctypes.c_uint64, ctypes.c_uint32,
+                                          P, P, P, P, ctypes.c_int]
         self.lib = lib
+
+    def philox(self, ctr, key):
+        """Philox4x32-10 of a 4-word counter under a 2-word key."""
+        c = np.ascontiguousarray(ctr, dtype=np.uint32).reshape(4)
+        k = np.ascontiguousarray(key, dtype=np.uint32).reshape(2)
+        out = np.empty(4, np.uint32)
+        self.lib.oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+        return out
+
+    def exp_draw(self, seed, counter, row, v):
+        """(E, U): the exponential draw of vocabulary entry v at position row
+        and the uniform it comes from."""
+        u = ctypes.c_double()
+        e = self.lib.oracle_exp_draw(int(seed), int(counter), int(row), int(v), ctypes.byref(u))
+        return e, u.value
+
+    def row_sample(self, hidden, W, rows, tau, seed, counter, nthreads: int = 0):
+        """Sampled candidates of ``rows``: dict with cand, conf, logp, keygap."""
+        h, dt_h = _as_input(hidden)
+        w, dt_w = _as_input(W)
+        if dt_h != dt_w:
+            raise TypeError("hidden and W must share a dtype")
+        M, d = h.shape
+        V, d2 = w.shape
+        if d != d2:
+            raise ValueError("hidden is [M, %d] but W is [V, %d]" % (d, d2))
+        if rows is None:
+            rows = np.arange(M, dtype=np.int64)
+        rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64)).reshape(-1)
+        if rows.size and (rows.min() < 0 or rows.max() >= M):
+            raise IndexError("row index out of range")
+        n = rows.size
+        out = {k: np.empty(n, np.float64) for k in ("conf", "logp", "keygap")}
+        out["cand"] = np.empty(n, np.int32)
+        rc = self.lib.oracle_row_sample(_ptr(h), _ptr(w), dt_h, d, V, _ptr(rows), n,
+                                        float(tau), int(seed), int(counter),
+                                        _ptr(out["cand"]), _ptr(out["conf"]),
+                                        _ptr(out["logp"]), _ptr(out["keygap"]), int(nthreads))
+        if rc == -2:
+            raise FloatingPointError("non-finite logit")
+        if rc != 0:
+            raise ValueError("oracle_row_sample rejected its arguments (%d)" % rc)
+        return out
 
     def row_stats(self, hidden, W, rows=None, nthreads: int = 0):
         """Statistics of q(. | x_t) for ``rows`` of ``hidden`` ([M, d])
@@ -201,3 +258,15 @@ def select_ex(*a, **k):
 
 def step(*a, **k):
     return default().step(*a, **k)
+
+
+def row_sample(*a, **k):
+    return default().row_sample(*a, **k)
+
+
+def philox(*a, **k):
+    return default().philox(*a, **k)
+
+
+def exp_draw(*a, **k):
+    return default().exp_draw(*a, **k)

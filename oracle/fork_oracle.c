@@ -30,6 +30,30 @@ static double widen(const void* base, int dtype, int64_t idx) {
   return (double)((const float*)base)[idx];
 }
 
+/* Logits of position r, z_v = <h_r, W_v>, accumulated with j ascending.
+ * Returns 0, or -2 when a logit is not finite. */
+static int logits(const void* hidden, const void* W, int dtype, int64_t d,
+                  int64_t V, int64_t r, double* z) {
+  for (int64_t v = 0; v < V; ++v) {
+    double acc = 0.0;
+    for (int64_t j = 0; j < d; ++j)
+      acc += widen(hidden, dtype, r * d + j) * widen(W, dtype, v * d + j);
+    if (!isfinite(acc)) return -2;
+    z[v] = acc;
+  }
+  return 0;
+}
+
+/* log sum_v exp(z_v), shifted by the maximum so that exp() cannot overflow */
+static double log_normaliser(const double* z, int64_t V) {
+  double zmax = z[0];
+  for (int64_t v = 1; v < V; ++v)
+    if (z[v] > zmax) zmax = z[v];
+  double sum = 0.0;
+  for (int64_t v = 0; v < V; ++v) sum += exp(z[v] - zmax);
+  return zmax + log(sum);
+}
+
 /* Statistics of q(. | x_t) for one position, from the definitions in Section 2
  * (the model's per-position categorical, the greedy candidate and its
  * confidence) and Section 3.1 (token entropy).  Returns 0, or -2 when a logit
@@ -38,23 +62,14 @@ static int one_row(const void* hidden, const void* W, int dtype, int64_t d,
                    int64_t V, int64_t r, double* z, double* conf,
                    double* entropy, double* logp, double* lse, int32_t* amax,
                    double* gap) {
-  /* logits z_v = <h_r, W_v>, accumulated with j ascending */
-  for (int64_t v = 0; v < V; ++v) {
-    double acc = 0.0;
-    for (int64_t j = 0; j < d; ++j)
-      acc += widen(hidden, dtype, r * d + j) * widen(W, dtype, v * d + j);
-    if (!isfinite(acc)) return -2;
-    z[v] = acc;
-  }
+  const int rc = logits(hidden, W, dtype, d, V, r, z);
+  if (rc) return rc;
   /* greedy candidate: the lowest index attaining the maximum logit */
   int64_t a = 0;
   for (int64_t v = 1; v < V; ++v)
     if (z[v] > z[a]) a = v;
   double zmax = z[a];
-  /* log-normaliser, shifted by the maximum so that exp() cannot overflow */
-  double sum = 0.0;
-  for (int64_t v = 0; v < V; ++v) sum += exp(z[v] - zmax);
-  double log_norm = zmax + log(sum);
+  double log_norm = log_normaliser(z, V);
   /* entropy -sum q log q with log q_v = z_v - log_norm */
   double h = 0.0;
   for (int64_t v = 0; v < V; ++v) {
@@ -115,6 +130,123 @@ int oracle_row_stats(const void* hidden, const void* W, int dtype, int64_t d,
   (void)nthreads;
   return status;
 }
+
+/* ---------------------------------------------------------------- sampling */
+
+/* One Philox round: two 32x32 -> 64-bit products, their halves exchanged and
+ * mixed with the other two counter words and the round key. */
+static void philox_round(uint32_t c[4], const uint32_t k[2]) {
+  const uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+  const uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+  const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+  const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+  const uint32_t n0 = hi1 ^ c[1] ^ k[0];
+  const uint32_t n2 = hi0 ^ c[3] ^ k[1];
+  c[0] = n0;
+  c[1] = lo1;
+  c[2] = n2;
+  c[3] = lo0;
+}
+
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                          uint32_t out[4]) {
+  uint32_t c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+  uint32_t k[2] = {key[0], key[1]};
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {  /* Weyl sequence of round keys */
+      k[0] += 0x9E3779B9u;
+      k[1] += 0xBB67AE85u;
+    }
+    philox_round(c, k);
+  }
+  memcpy(out, c, sizeof c);
+}
+
+double oracle_exp_draw(uint64_t seed, uint32_t counter, int64_t row, int64_t v,
+                       double* u) {
+  const uint32_t ctr[4] = {(uint32_t)(v / 4), (uint32_t)row, counter, 0u};
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t w[4];
+  oracle_philox4x32_10(ctr, key, w);
+  const double U = ldexp(2.0 * (double)(w[v % 4] >> 9) + 1.0, -24);
+  if (u) *u = U;
+  return -log1p(-U);
+}
+
+/* The drawn candidate of one position: the Gumbel-perturbed,
+ * temperature-scaled logits and their maximiser. */
+static int one_sample(const void* hidden, const void* W, int dtype, int64_t d,
+                      int64_t V, int64_t r, double tau, uint64_t seed,
+                      uint32_t counter, double* z, int32_t* cand, double* conf,
+                      double* logp, double* keygap) {
+  const int rc = logits(hidden, W, dtype, d, V, r, z);
+  if (rc) return rc;
+  const double log_norm = log_normaliser(z, V);
+  /* keys z_v / tau + g_v with g_v = -log E_v; best and runner-up */
+  int64_t a = -1;
+  double best = -INFINITY, second = -INFINITY;
+  for (int64_t v = 0; v < V; ++v) {
+    const double key = z[v] / tau - log(oracle_exp_draw(seed, counter, r, v, NULL));
+    if (a < 0 || key > best) {
+      second = best;
+      best = key;
+      a = v;
+    } else if (key > second) {
+      second = key;
+    }
+  }
+  const double log_q = z[a] - log_norm;  /* untempered log q of the draw */
+  if (cand) *cand = (int32_t)a;
+  if (conf) *conf = exp(log_q);
+  if (logp) *logp = log_q;
+  if (keygap) *keygap = (V > 1) ? (best - second) : 0.0;
+  return 0;
+}
+
+int oracle_row_sample(const void* hidden, const void* W, int dtype, int64_t d,
+                      int64_t V, const int64_t* rows, int64_t nrows,
+                      double tau, uint64_t seed, uint32_t counter,
+                      int32_t* cand, double* conf, double* logp,
+                      double* keygap, int nthreads) {
+  if (!hidden || !W || !rows || d <= 0 || V <= 0 || V > INT32_MAX || nrows < 0)
+    return -1;
+  if (dtype != ORACLE_BF16 && dtype != ORACLE_F32) return -1;
+  if (!(tau > 0.0) || !isfinite(tau)) return -1;
+  int status = 0;
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#pragma omp parallel num_threads(nthreads)
+#endif
+  {
+    double* z = (double*)malloc((size_t)V * sizeof(double));
+    if (!z) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      status = -1;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t i = 0; i < nrows; ++i) {
+        int rc = one_sample(hidden, W, dtype, d, V, rows[i], tau, seed, counter, z,
+                            cand ? cand + i : NULL, conf ? conf + i : NULL,
+                            logp ? logp + i : NULL, keygap ? keygap + i : NULL);
+        if (rc) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+          status = rc;
+        }
+      }
+      free(z);
+    }
+  }
+  (void)nthreads;
+  return status;
+}
+
+/* ---------------------------------------------------------------- selection */
 
 /* The single position committed on a fallback step, among the masked
  * positions of [s, e) of sequence row `base`. */

@@ -94,6 +94,46 @@ int oracle_select_ex(int32_t B, int32_t L, int32_t block_len,
                      int32_t* tokens, uint8_t* mask, int32_t* block_start,
                      int32_t* fallback, int32_t* ncommit);
 
+/*
+ * Philox4x32-10, the counter-based generator of Salmon, Moraes, Dror and
+ * Shaw ("Parallel random numbers: as easy as 1, 2, 3", SC'11): ten rounds of
+ * the 4x32 Philox S-box on the counter, the key bumped by the Weyl constants
+ * between rounds.
+ */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                          uint32_t out[4]);
+
+/*
+ * The random draw attached to vocabulary entry v of position `row` in the
+ * sampled-candidate step (`counter` is the caller's step counter):
+ *   w = Philox4x32-10(ctr = (v / 4, row, counter, 0),
+ *                     key = (seed mod 2^32, seed / 2^32))[v mod 4]
+ *   U = (2 * (w >> 9) + 1) * 2^-24        (uniform on an odd grid in (0, 1))
+ *   E = -log(1 - U)                       (standard exponential)
+ * Returns E; *u (may be NULL) receives U.
+ */
+double oracle_exp_draw(uint64_t seed, uint32_t counter, int64_t row, int64_t v,
+                       double* u);
+
+/*
+ * Sampled candidates at temperature tau > 0 (Section 2: the candidate is
+ * drawn from q^k(. | x_t; tau), the softmax of z / tau), by the Gumbel-max
+ * property: -log E_v is a standard Gumbel variable, so
+ *   cand   = argmax_v  z_v / tau - log E_v            (lowest v on ties)
+ * is distributed as softmax(z / tau).  With lse = log sum_v exp(z_v):
+ *   conf   = exp(z_cand - lse)      (untempered q of the drawn token)
+ *   logp   = z_cand - lse
+ *   keygap = key_cand - max_{v != cand} key_v          (0 if V == 1)
+ * Rows, outputs and return codes as in oracle_row_stats; -1 also when tau is
+ * not a positive finite number.
+ */
+int oracle_row_sample(const void* hidden, const void* W, int dtype,
+                      int64_t d, int64_t V,
+                      const int64_t* rows, int64_t nrows,
+                      double tau, uint64_t seed, uint32_t counter,
+                      int32_t* cand, double* conf, double* logp,
+                      double* keygap, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

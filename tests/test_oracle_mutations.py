@@ -40,6 +40,16 @@ MUTATIONS = {
     "random_off_by_one": ("if (mask[base + k] && j-- == 0) return k;", "if (mask[base + k] && --j == 0) return k;"),
     "random_rounds_up": ("int32_t j = (int32_t)prod;", "int32_t j = (int32_t)(prod + 0.5f);"),
     "no_skip_forward": ("s += block_len;", "break;"),
+    "philox_multiplier": ("0xD2511F53u", "0xD2511F55u"),
+    "philox_no_key_bump": ("k[1] += 0xBB67AE85u;", ""),
+    "philox_words_swapped": ("c[0] = n0;\n  c[1] = lo1;", "c[0] = lo1;\n  c[1] = n0;"),
+    "draw_counter_layout": ("{(uint32_t)(v / 4), (uint32_t)row, counter, 0u}",
+                            "{(uint32_t)(v / 4), counter, (uint32_t)row, 0u}"),
+    "gumbel_sign": ("z[v] / tau - log(oracle_exp_draw(", "z[v] / tau + log(oracle_exp_draw("),
+    "temperature_multiplies": ("z[v] / tau - log(", "z[v] * tau - log("),
+    "sample_logq_drops_logit": ("const double log_q = z[a] - log_norm;",
+                              "const double log_q = log_norm - log_norm;"),
+    "keygap_stale_second": ("      second = best;\n      best = key;", "      best = key;"),
 }
 
 
@@ -61,6 +71,11 @@ def _checks(orc):
         lambda: pins.test_fast_fallback_tie_takes_lowest_position(orc),
         lambda: pins.test_fallback_ablations_hand_worked(orc),
         lambda: pins.test_fallback_ablation_properties(orc, 0),
+        lambda: pins.test_philox_known_answers(orc),
+        lambda: pins.test_exp_draw_layout_and_law(orc),
+        lambda: pins.test_sample_frequencies_follow_tempered_softmax(orc, 0.5),
+        lambda: pins.test_sample_low_temperature_is_greedy(orc),
+        lambda: pins.test_sample_brute_force_keys(orc),
     ]
     failed = 0
     for c in calls:

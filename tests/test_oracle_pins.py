@@ -417,3 +417,108 @@ def test_select_ex_rejects_missing_inputs(orc):
         orc.select_ex(z, a, a, m, bs, 1, 4, 4, 0.5, oracle.RULE_RANDOM)
     with pytest.raises(ValueError):
         orc.select_ex(z, a, a, m, bs, 1, 4, 4, 0.5, 9)
+
+
+# ------------------------------------------------------------ sampled candidates
+#
+# Section 2 draws the candidate from q(. | x_t; tau).  The oracle uses the
+# Gumbel-max property with Philox4x32-10 draws; the pins below tie the
+# generator to its published known answers, the draw to the exponential law,
+# and the candidate to softmax(z / tau) in distribution, to the greedy
+# candidate as tau -> 0, and to brute-force keys on tiny inputs.
+
+def _kat():
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.json")) as f:
+        return json.load(f)["vectors"]
+
+
+def test_philox_known_answers(orc):
+    for vec in _kat():
+        h = lambda xs: [int(x, 16) for x in xs]
+        out = orc.philox(h(vec["ctr"]), h(vec["key"]))
+        assert [int(x) for x in out] == h(vec["out"])
+
+
+def test_exp_draw_layout_and_law(orc):
+    """U comes from word v % 4 of Philox(ctr = (v/4, row, counter, 0), key =
+    (seed lo, seed hi)) on the odd grid of (0, 1); E = -log(1 - U) follows
+    the standard exponential law (Kolmogorov-Smirnov on 60000 draws)."""
+    seed, counter = 0x0123456789ABCDEF, 41
+    for row, v in [(0, 0), (5, 3), (77, 126463), (3, 9)]:
+        e, u = orc.exp_draw(seed, counter, row, v)
+        w = orc.philox([v // 4, row, counter, 0], [seed & 0xFFFFFFFF, seed >> 32])[v % 4]
+        assert u == (2 * (int(w) >> 9) + 1) * 2.0 ** -24
+        assert 0.0 < u < 1.0 and e == -math.log1p(-u)
+    draws = np.array([orc.exp_draw(7, 3, r, v)[0] for r in range(60) for v in range(1000)])
+    assert draws.min() > 0.0
+    assert scipy.stats.kstest(draws, "expon").pvalue > 1e-3
+
+
+@pytest.mark.parametrize("tau", [0.5, 1.0, 2.0])
+def test_sample_frequencies_follow_tempered_softmax(orc, tau):
+    """40000 positions holding the same hidden row (independent draws, since
+    the row index is part of the counter): candidate frequencies against
+    softmax(z / tau), chi-square."""
+    rng = np.random.default_rng(11)
+    d, V, n = 4, 6, 40000
+    W = rng.standard_normal((V, d)).astype(np.float32)
+    h1 = rng.standard_normal(d).astype(np.float32)
+    out = orc.row_sample(np.tile(h1, (n, 1)), W, None, tau, seed=12345, counter=7)
+    z = W.astype(np.float64) @ h1.astype(np.float64)
+    p = np.exp(z / tau - (z / tau).max())
+    p /= p.sum()
+    counts = np.bincount(out["cand"], minlength=V)
+    assert scipy.stats.chisquare(counts, p * n).pvalue > 1e-4
+
+
+def test_sample_low_temperature_is_greedy(orc):
+    """tau -> 0: z / tau separates the top logit by far more than the
+    perturbations can move it (|log E| < 17 on this grid)."""
+    rng = np.random.default_rng(5)
+    h = rng.standard_normal((40, 64)).astype(np.float32)
+    W = rng.standard_normal((300, 64)).astype(np.float32)
+    st = orc.row_stats(h, W)
+    out = orc.row_sample(h, W, None, 1e-3, seed=9, counter=0)
+    clear = st["gap"] > 0.05
+    assert clear.sum() >= 30
+    assert np.array_equal(out["cand"][clear], st["argmax"][clear])
+    np.testing.assert_allclose(out["conf"][clear], st["conf"][clear], rtol=1e-12)
+
+
+def test_sample_brute_force_keys(orc):
+    """Candidate, key gap, confidence and log-probability against keys built
+    here from numpy logits and the generator's draws."""
+    rng = np.random.default_rng(8)
+    d, V, tau = 16, 50, 0.8
+    h = rng.standard_normal((6, d)).astype(np.float32)
+    W = rng.standard_normal((V, d)).astype(np.float32)
+    out = orc.row_sample(h, W, None, tau, seed=77, counter=3)
+    z = h.astype(np.float64) @ W.astype(np.float64).T
+    for r in range(h.shape[0]):
+        key = np.array([z[r, v] / tau - math.log(orc.exp_draw(77, 3, r, v)[0])
+                        for v in range(V)])
+        order = np.argsort(-key, kind="stable")
+        assert out["cand"][r] == order[0]
+        assert out["keygap"][r] == pytest.approx(key[order[0]] - key[order[1]], abs=1e-12)
+        lse = z[r].max() + math.log(np.exp(z[r] - z[r].max()).sum())
+        assert out["logp"][r] == pytest.approx(z[r, order[0]] - lse, abs=1e-12)
+        assert out["conf"][r] == pytest.approx(math.exp(z[r, order[0]] - lse), rel=1e-12)
+
+
+def test_sample_draws_change_with_seed_counter_and_row(orc):
+    rng = np.random.default_rng(2)
+    h = np.tile(rng.standard_normal(8).astype(np.float32), (200, 1))
+    W = (0.1 * rng.standard_normal((64, 8))).astype(np.float32)  # nearly flat q
+    a = orc.row_sample(h, W, None, 1.0, seed=1, counter=0)["cand"]
+    assert len(set(a.tolist())) > 20                      # rows differ
+    b = orc.row_sample(h, W, None, 1.0, seed=1, counter=1)["cand"]
+    c = orc.row_sample(h, W, None, 1.0, seed=2, counter=0)["cand"]
+    assert (a != b).mean() > 0.8 and (a != c).mean() > 0.8
+    assert np.array_equal(a, orc.row_sample(h, W, None, 1.0, seed=1, counter=0)["cand"])
+
+
+@pytest.mark.parametrize("tau", [0.0, -1.0, float("inf"), float("nan")])
+def test_sample_rejects_bad_temperature(orc, tau):
+    h = np.ones((1, 4), np.float32)
+    with pytest.raises(ValueError):
+        orc.row_sample(h, h, None, tau, seed=0, counter=0)
