@@ -14,7 +14,8 @@ events recorded around that kernel alone on the stream it runs on.
 `cpu_baseline` times the binary64 CPU oracle on a bounded sample of rows of
 the same workload and scales it to steps per second.  `active_rows_mode`
 times the same decode with the LM head restricted to each sequence's active
-block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload.
+block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload; `drawn_candidates`
+times both modes with candidates drawn at sampling temperature 0.8.
 """
 import argparse
 import ctypes
@@ -105,6 +106,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-active-rows", action="store_true",
                     help="skip the extra timing of the active-block-only LM head")
+    ap.add_argument("--no-drawn", action="store_true",
+                    help="skip the extra timings with candidates drawn at temperature 0.8")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -157,7 +160,7 @@ def main():
         bs.copy_(bs0.to(dev))
         torch.cuda.synchronize()
 
-    def timed(rows_mode, steps, warmup):
+    def timed(rows_mode, steps, warmup, temperature=0.0):
         """Warm up, restart the decode, then time `steps` steps: total time
         from torch events on the current stream, LM-head time per step from
         HIP events the library records around that kernel on the same
@@ -170,7 +173,8 @@ def main():
 
         def step(i, events=None):
             _binding.fork_step_ex(hs[i % n_batches], W, tok, msk, bs, BL, cfg.tau, conf, ent,
-                                  logp, fb, B=B, L=L, events=events, rows_mode=rows_mode)
+                                  logp, fb, B=B, L=L, events=events, rows_mode=rows_mode,
+                                  temperature=temperature, seed=0x5EED, counter=i)
 
         for i in range(warmup):
             step(i)
@@ -254,6 +258,21 @@ def main():
                          "algorithmic_bytes_per_launch": a_bytes,
                          "mfma_frac": 2.0 * Ma * d * V / (a_lm_ms * 1e-3) / 1e12
                                       / PEAK_BF16_TFLOPS}}
+    if not args.no_drawn:
+        # Candidates drawn at sampling temperature 0.8 (Gumbel-max over
+        # Philox4x32-10 draws for the active blocks' positions).
+        drawn = {"temperature": 0.8}
+        for label, mode, kernel in (("all_rows", _binding.FORK_ROWS_ALL, "gemm_stats_bf16_draw_kernel"),
+                                    ("active_rows", _binding.FORK_ROWS_ACTIVE,
+                                     "gemm_stats_bf16_rows_draw_kernel")):
+            print("bench: timing %d steps, drawn candidates, %s" % (args.steps, label),
+                  file=sys.stderr, flush=True)
+            d_total, d_lm, _ = timed(mode, args.steps, args.warmup, temperature=0.8)
+            reset()
+            drawn[label] = {"ms_per_step": d_total / args.steps,
+                            "steps_per_s": 1000.0 * args.steps / d_total,
+                            "lmhead_ms": sum(d_lm) / len(d_lm), "kernel": kernel}
+        out["drawn_candidates"] = drawn
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)

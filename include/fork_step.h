@@ -164,14 +164,31 @@ typedef struct fork_step_args {
      FORK_RULE_RANDOM (required by that rule, ignored by the others). */
   const float* fallback_uniform;
   int32_t rows_mode;       /* FORK_ROWS_*; fork_step uses FORK_ROWS_ALL        */
+  /* Drawn candidates (Section 2: the candidate of position k is drawn from
+     q^k(. | x_t; tau), the softmax of the logits divided by the sampling
+     temperature).  0 (fork_step's value) keeps the greedy candidate.  With
+     sample_temperature > 0 the candidates of the active blocks' positions
+     are drawn by the Gumbel-max property: cand = argmax_v z_v / tau - log E_v
+     with E_v = -log(1 - U_v), U_v = (2 (w >> 9) + 1) 2^-24 and w word v % 4
+     of Philox4x32-10 (Salmon et al., SC'11) at counter
+     (v / 4, b * L + k, sample_counter, 0) under key (sample_seed mod 2^32,
+     sample_seed / 2^32); ties go to the lower v.  out_conf and out_logp of
+     such a position are q(cand) and log q(cand) of the untempered q (the
+     confidence of Algorithm 2); out_entropy and out_lse are unchanged.
+     Other positions keep the greedy candidate and its statistics.  Draws do
+     not depend on rows_mode.  Must be finite and >= 0 (FORK_EINVAL). */
+  float sample_temperature;
+  uint32_t sample_counter; /* per-step counter of the draws (e.g. step index) */
+  uint64_t sample_seed;    /* key of the draws                                 */
 } fork_step_args;
 
 /* fork_step with the extras above.  Same return codes. */
 int fork_step_ex(const fork_step_args* args);
 
-/* Device workspace bytes a step with these sizes needs (per-tile partial
-   statistics, the per-position candidates and the active-row list); 0 if the
-   sizes are invalid. */
+/* Device workspace bytes a step with these sizes needs in any mode (per-tile
+   partial statistics, the per-position candidates, the active-row list, and
+   the per-tile drawn candidates when sample_temperature > 0); 0 if the sizes
+   are invalid. */
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
 
 /* Description of the last non-OK return on the calling thread ("" if none).

@@ -48,6 +48,8 @@ class ForkStepArgs(ctypes.Structure):
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("ev_lmhead_begin", _P), ("ev_lmhead_end", _P),
         ("fallback_uniform", _P), ("rows_mode", _I32),
+        ("sample_temperature", ctypes.c_float), ("sample_counter", ctypes.c_uint32),
+        ("sample_seed", ctypes.c_uint64),
     ]
 
 
@@ -130,7 +132,8 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
                  B: int, L: int, out_lse=None, out_argmax=None, out_ncommit=None,
                  out_commit_pos=None, rule: int = FORK_RULE_LEFTMOST,
                  workspace: Optional[torch.Tensor] = None, stream=None,
-                 events=None, fallback_uniform=None, rows_mode: int = FORK_ROWS_ALL) -> None:
+                 events=None, fallback_uniform=None, rows_mode: int = FORK_ROWS_ALL,
+                 temperature: float = 0.0, seed: int = 0, counter: int = 0) -> None:
     """fork_step_ex of the C ABI; optional outputs may be None.  ``events``
     is an optional pair of raw hipEvent_t handles (ints) recorded around the
     LM-head kernel."""
@@ -178,6 +181,9 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
         a.ev_lmhead_begin, a.ev_lmhead_end = events
     a.fallback_uniform = _opt(fallback_uniform, "fallback_uniform", torch.float32, B, device)
     a.rows_mode = int(rows_mode)
+    a.sample_temperature = float(temperature)
+    a.sample_counter = int(counter) & 0xFFFFFFFF
+    a.sample_seed = int(seed) & 0xFFFFFFFFFFFFFFFF
     rc = lib().fork_step_ex(ctypes.byref(a))
     if rc != FORK_OK:
         raise ForkError(rc, lib().fork_last_error().decode())

@@ -35,20 +35,24 @@ int fail(int code, const char* fmt, ...) {
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Workspace layout: [partials: nvt*M float4][argmax: M int32][rows: M int32].
+// Workspace layout: [partials: nvt*M float4][argmax: M int32]
+// [rows: M int32 (active-row list or row map)][drawn partials: nvt*M float4,
+// only when candidates are drawn].
 struct Layout {
-  size_t partial_off, argmax_off, rows_off, total;
+  size_t partial_off, argmax_off, rows_off, spartial_off, total;
 };
 
-bool layout_for(int32_t B, int32_t L, int32_t V, Layout* out) {
+bool layout_for(int32_t B, int32_t L, int32_t V, bool sampling, Layout* out) {
   if (B <= 0 || L <= 0 || V <= 0) return false;
   const long long M = (long long)B * L;
   if (M > 0x7fffffffLL) return false;
   const size_t nvt = (size_t)fork::num_vocab_tiles(V);
+  const size_t part = align_up(nvt * (size_t)M * sizeof(float4));
   out->partial_off = 0;
-  out->argmax_off = align_up(nvt * (size_t)M * sizeof(float4));
+  out->argmax_off = part;
   out->rows_off = out->argmax_off + align_up((size_t)M * sizeof(int32_t));
-  out->total = out->rows_off + align_up((size_t)M * sizeof(int32_t));
+  out->spartial_off = out->rows_off + align_up((size_t)M * sizeof(int32_t));
+  out->total = out->spartial_off + (sampling ? part : 0);
   return true;
 }
 
@@ -119,6 +123,8 @@ int validate(const fork_step_args* a) {
   if (a->rows_mode == FORK_ROWS_ACTIVE &&
       (long long)a->B * a->L * a->d * (a->dtype == FORK_BF16 ? 2 : 4) >= (1LL << 31))
     return fail(FORK_EUNSUPPORTED, "FORK_ROWS_ACTIVE needs B*L*d*element_size < 2^31");
+  if (!(a->sample_temperature >= 0.0f) || !isfinite(a->sample_temperature))
+    return fail(FORK_EINVAL, "sample_temperature must be finite and >= 0");
   return FORK_OK;
 }
 
@@ -129,8 +135,9 @@ extern "C" {
 int fork_step_ex(const fork_step_args* a) {
   int rc = validate(a);
   if (rc != FORK_OK) return rc;
+  const bool sampling = a->sample_temperature > 0.0f;
   Layout lay;
-  if (!layout_for(a->B, a->L, a->V, &lay)) return fail(FORK_EINVAL, "invalid sizes");
+  if (!layout_for(a->B, a->L, a->V, sampling, &lay)) return fail(FORK_EINVAL, "invalid sizes");
   void* ws = a->workspace;
   if (ws) {
     if (a->workspace_bytes < lay.total)
@@ -147,14 +154,26 @@ int fork_step_ex(const fork_step_args* a) {
   float4* partials = reinterpret_cast<float4*>(static_cast<char*>(ws) + lay.partial_off);
   int32_t* argmax = a->out_argmax ? a->out_argmax
                                   : reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.argmax_off);
-  int32_t* rowlist = active ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.rows_off)
-                            : nullptr;
+  // one int32 region: the active-row list (FORK_ROWS_ACTIVE) or, when
+  // drawing over all rows, the map of rows whose candidates are drawn
+  int32_t* rows = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lay.rows_off);
+  int32_t* rowlist = active ? rows : nullptr;
+  int32_t* rowmap = (!active && sampling) ? rows : nullptr;
+  fork::SampleArgs sa = {};
+  if (sampling) {
+    sa.row = active ? rowlist : rowmap;
+    sa.partials = reinterpret_cast<float4*>(static_cast<char*>(ws) + lay.spartial_off);
+    sa.inv_tau = 1.0f / a->sample_temperature;
+    sa.key0 = (uint32_t)a->sample_seed;
+    sa.key1 = (uint32_t)(a->sample_seed >> 32);
+    sa.counter = a->sample_counter;
+  }
   hipStream_t stream = static_cast<hipStream_t>(a->stream);
 
   hipError_t e;
-  if (active) {
+  if (rowlist || rowmap) {
     e = fork::launch_active_rows(a->B, a->L, a->block_len, a->mask, a->block_start, rowlist,
-                                 stream);
+                                 rowmap, stream);
     if (e != hipSuccess) return fail(FORK_EHIP, "active_rows launch: %s", hipGetErrorString(e));
   }
   if (a->ev_lmhead_begin) {
@@ -162,14 +181,14 @@ int fork_step_ex(const fork_step_args* a) {
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_gemm_stats(a->hidden, a->W_head, a->dtype == FORK_BF16, M, a->d, a->V,
-                              partials, rowlist, Mh, stream);
+                              partials, rowlist, Mh, sa, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "gemm_stats launch: %s", hipGetErrorString(e));
   if (a->ev_lmhead_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_end), stream);
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_merge(partials, M, nvt, a->out_conf, a->out_entropy, a->out_logp, a->out_lse,
-                         argmax, rowlist, stream);
+                         argmax, rowlist, sa.row, sa.partials, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
   e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf,
                           a->out_entropy, a->fallback_uniform, argmax, a->tokens, a->mask,
@@ -216,7 +235,7 @@ int fork_step(const void* hidden, const void* W_head, int32_t* tokens, uint8_t* 
 
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V) {
   Layout lay;
-  return layout_for(B, L, V, &lay) ? lay.total : 0;
+  return layout_for(B, L, V, /*sampling=*/true, &lay) ? lay.total : 0;
 }
 
 const char* fork_last_error(void) { return g_err; }

@@ -21,6 +21,18 @@ struct Partial {
   int idx;
 };
 
+// Drawn candidates at a sampling temperature tau > 0 (Gumbel-max over
+// Philox4x32-10 draws).  row[p] is the row index that keys the draws of
+// LM-head position p, or -1 for a position that keeps the greedy candidate;
+// a null `row` disables drawing.  partials[vt * M + p] receives, for each
+// drawn position, {best key, its vocabulary index (int32 bits), its logit, 0}.
+struct SampleArgs {
+  const int32_t* row;
+  float4* partials;
+  float inv_tau;
+  uint32_t key0, key1, counter;
+};
+
 inline int num_vocab_tiles(int V) { return (V + kTileV - 1) / kTileV; }
 inline int num_pos_tiles(int M) { return (M + kTileP - 1) / kTileP; }
 
@@ -29,21 +41,27 @@ inline int num_pos_tiles(int M) { return (M + kTileP - 1) / kTileP; }
 // p, or with a row list hidden row rowlist[p] (-1 = none) out of Mh rows.
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16,
                              int M, int d, int V, float4* partials,
-                             const int32_t* rowlist, int Mh, hipStream_t stream);
+                             const int32_t* rowlist, int Mh, const SampleArgs& sample,
+                             hipStream_t stream);
 
 // Merge the partials of each position over all vocabulary tiles into the
 // per-position results (position p lands in row p, or rowlist[p] if a row
-// list is given; -1 = dropped).  lse may be null.
+// list is given; -1 = dropped).  lse may be null.  Positions with
+// sample_row[p] >= 0 (sample_row may be null) take the drawn candidate from
+// spartials, with the untempered confidence and log-probability of it.
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse,
-                        int32_t* argmax, const int32_t* rowlist, hipStream_t stream);
+                        int32_t* argmax, const int32_t* rowlist,
+                        const int32_t* sample_row, const float4* spartials,
+                        hipStream_t stream);
 
 // Rows of each sequence's active block (the same skip-forward as the
 // selection): rowlist[b * block_len + i] = b * L + s_b + i, -1 past the block
-// end or for sequences with nothing to commit.
+// end or for sequences with nothing to commit.  rowmap (B * L entries) holds
+// r for the rows of the active blocks and -1 elsewhere.  Either may be null.
 hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
                               const int32_t* block_start, int32_t* rowlist,
-                              hipStream_t stream);
+                              int32_t* rowmap, hipStream_t stream);
 
 // Unmasking rule per sequence, in place.  ncommit / commit_pos may be null;
 // entropy is read by the highest-entropy rule, uniform by the random rule.

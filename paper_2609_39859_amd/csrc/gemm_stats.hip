@@ -38,6 +38,13 @@
 // the buffer loads of later stages are spread over the stage in small groups
 // so that no wave stalls its MFMA stream behind a burst of loads.
 // fp32 path (small problems): register-staged double buffer.
+//
+// Drawn candidates (sampling temperature tau > 0, Section 2): for the
+// positions the caller marks, the epilogue also keeps the maximiser of the
+// Gumbel-perturbed keys z_v / tau - log E_v, where E_v = -log(1 - U_v) is an
+// exponential draw built from Philox4x32-10 (Salmon et al., SC'11) at
+// counter (v / 4, row, step counter, 0): one generator call serves the four
+// consecutive vocabulary entries a lane holds in one accumulator group.
 #include "fork_kernels.h"
 
 #include <math.h>
@@ -98,6 +105,38 @@ __device__ __forceinline__ float4 merge2(float4 a, float4 b) {
   return r;
 }
 
+// Philox4x32-10: ten rounds of the 4x32 S-box (two 32 x 32 -> 64-bit
+// products whose halves are exchanged and mixed with the other counter words
+// and the round key), the key advanced by the Weyl constants between rounds.
+// Each product is one 32 x 32 -> 64-bit multiply (v_mad_u64_u32).
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1,
+                   (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// Gumbel key of one logit: z / tau - log E with E = -log(1 - U) and U on the
+// odd grid (2 (w >> 9) + 1) 2^-24 of (0, 1).  1 - U is exact in binary32, so
+// E comes from the hardware base-2 logarithm, except below U = 2^-7, where
+// the series U + U^2/2 + U^3/3 + U^4/4 (relative error < U^4/5 < 2^-30)
+// avoids the cancellation of a logarithm near 1.  The key carries a relative
+// error of about 1e-6 in E, far below the logit rounding.
+__device__ __forceinline__ float gumbel_key(float z, float inv_tau, uint32_t w) {
+  constexpr float kLn2 = 0.6931471805599453f;
+  const float u = (float)(2u * (w >> 9) + 1u) * 0x1p-24f;
+  const float series = u * fmaf(u, fmaf(u, fmaf(u, 0.25f, 1.0f / 3.0f), 0.5f), 1.0f);
+  const float viaLog = -__builtin_amdgcn_logf(1.0f - u) * kLn2;
+  const float e = u < 0x1p-7f ? series : viaLog;
+  return fmaf(z, inv_tau, -__builtin_amdgcn_logf(e) * kLn2);
+}
+
 // Vocabulary index held by accumulator element `e` of MFMA tile `i` in this
 // lane (32x32 output layout: column = lane % 32, row = 8*(e/4) + 4*(lane/32)
 // + e%4), relative to the wave's first vocabulary row.
@@ -107,10 +146,15 @@ __device__ __forceinline__ int acc_row(int i, int e, int lane) {
 
 // Per-(position, tile) statistics from the accumulators of one wave, combined
 // across the two vocabulary waves through LDS, stored to partials.
+// Drawn candidates (kDraw) go through a second LDS exchange and a second
+// partials array (see SampleArgs).
+template <bool kDraw>
 __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned char* smem, int tid,
                                          int lane, int wv, int wp, int vt, int v0, int p0, int M,
-                                         int V, float4* __restrict__ partials) {
+                                         int V, float4* __restrict__ partials,
+                                         const SampleArgs& sa) {
   float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
+  float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
   const int vbase = v0 + wv * 128;
   const bool full = v0 + kTileV <= V;
 #pragma unroll
@@ -154,13 +198,60 @@ __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned cha
     }
     s += __shfl_xor(s, 32);
     t += __shfl_xor(t, 32);
-    if (lane < 32)
-      red[wv * kTileP + wp * 64 + j * 32 + lane] = make_float4(m, s, t, __int_as_float(idx));
+    const int col = wp * 64 + j * 32 + (lane & 31);
+    if (lane < 32) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
+    if (kDraw) {
+      const int srow = p0 + col < M ? sa.row[p0 + col] : -1;
+      if (__ballot(srow >= 0)) {
+        float best = -INFINITY, bz = 0.f;
+        int bidx = 0x7fffffff;
+        if (srow >= 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int vq = vbase + acc_row(i, 4 * g, lane);  // multiple of 4
+              if (full || vq < V) {
+                const uint4 w = philox4x32_10(make_uint4((uint32_t)vq >> 2, (uint32_t)srow,
+                                                         sa.counter, 0u),
+                                              sa.key0, sa.key1);
+                const uint32_t words[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                  const float z = acc[i][j][4 * g + c];
+                  const float key = gumbel_key(z, sa.inv_tau, words[c]);
+                  if ((full || vq + c < V) && key > best) {
+                    best = key;
+                    bidx = vq + c;
+                    bz = z;
+                  }
+                }
+              }
+            }
+        }
+        const float ob = __shfl_xor(best, 32), oz = __shfl_xor(bz, 32);
+        const int oi = __shfl_xor(bidx, 32);
+        if (ob > best || (ob == best && oi < bidx)) {
+          best = ob;
+          bidx = oi;
+          bz = oz;
+        }
+        if (lane < 32) sred[wv * kTileP + col] = make_float4(best, __int_as_float(bidx), bz, 0.f);
+      }
+    }
   }
   __syncthreads();
   if (tid < kTileP) {
     const int r = p0 + tid;
-    if (r < M) partials[(size_t)vt * M + r] = merge2(red[tid], red[kTileP + tid]);
+    if (r < M) {
+      partials[(size_t)vt * M + r] = merge2(red[tid], red[kTileP + tid]);
+      if (kDraw && sa.row[r] >= 0) {
+        const float4 a = sred[tid], b = sred[kTileP + tid];
+        const bool take_a = a.x > b.x || (a.x == b.x && __float_as_int(a.y) < __float_as_int(b.y));
+        sa.partials[(size_t)vt * M + r] = make_float4(take_a ? a.x : b.x, take_a ? a.y : b.y,
+                                                      take_a ? a.z : b.z, 0.f);
+      }
+    }
   }
 }
 
@@ -180,10 +271,11 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
+template <bool kDraw>
 __device__ __forceinline__ void gemm_stats_bf16_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
     int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
-    int Mh) {
+    int Mh, const SampleArgs& sa) {
   // W ring: slots 0..2; hidden ring: slots 3..4
   __shared__ __attribute__((aligned(1024))) unsigned char smem[5 * kOperandBytes];
 
@@ -378,15 +470,16 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
-  epilogue(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials);
+  epilogue<kDraw>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa);
 }
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
 // 16-byte chunk.
+template <bool kDraw>
 __device__ __forceinline__ void gemm_stats_f32_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
     int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
-    int Mh) {
+    int Mh, const SampleArgs& sa) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * kOperandBytes];
 
   const int tid = threadIdx.x;
@@ -480,23 +573,37 @@ __device__ __forceinline__ void gemm_stats_f32_body(
     __syncthreads();
   }
 
-  epilogue(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials);
+  epilogue<kDraw>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa);
 }
 
 // Entry points: positions = hidden rows 0..M-1, or gathered through a row
-// list (the active-block rows).  Separate symbols keep the row-list
-// branches out of the dense kernel and the two apart in kernel traces.
+// list (the active-block rows); greedy candidates only, or drawn candidates
+// as well.  Separate symbols keep the row-list and drawing code out of the
+// dense greedy kernel and the variants apart in kernel traces.
 #define FORK_GEMM_ENTRIES(T)                                                                   \
   __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_kernel(                        \
       const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
       int d, int V, int nvt, int npt, float4* __restrict__ partials) {                         \
-    gemm_stats_##T##_body(hidden, W, M, d, V, nvt, npt, partials, nullptr, M);                 \
+    gemm_stats_##T##_body<false>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M,           \
+                                 SampleArgs{});                                                \
   }                                                                                            \
   __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_kernel(                   \
       const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
       int d, int V, int nvt, int npt, float4* __restrict__ partials,                           \
       const int32_t* __restrict__ rowlist, int Mh) {                                           \
-    gemm_stats_##T##_body(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh);                \
+    gemm_stats_##T##_body<false>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh,          \
+                                 SampleArgs{});                                                \
+  }                                                                                            \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_draw_kernel(                   \
+      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
+      int d, int V, int nvt, int npt, float4* __restrict__ partials, SampleArgs sa) {          \
+    gemm_stats_##T##_body<true>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M, sa);       \
+  }                                                                                            \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_draw_kernel(              \
+      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
+      int d, int V, int nvt, int npt, float4* __restrict__ partials,                           \
+      const int32_t* __restrict__ rowlist, int Mh, SampleArgs sa) {                            \
+    gemm_stats_##T##_body<true>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh, sa);      \
   }
 FORK_GEMM_ENTRIES(bf16)
 FORK_GEMM_ENTRIES(f32)
@@ -506,27 +613,32 @@ FORK_GEMM_ENTRIES(f32)
 
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M, int d, int V,
                              float4* partials, const int32_t* rowlist, int Mh,
-                             hipStream_t stream) {
+                             const SampleArgs& sample, hipStream_t stream) {
   const int nvt = num_vocab_tiles(V);
   const int npt = num_pos_tiles(M);
   const dim3 grid((unsigned)(nvt * npt)), block(kThreads);
   const auto* h = static_cast<const unsigned char*>(hidden);
   const auto* w = static_cast<const unsigned char*>(W);
-  if (rowlist) {
-    if (bf16)
-      hipLaunchKernelGGL(gemm_stats_bf16_rows_kernel, grid, block, 0, stream, h, w, M, d, V, nvt,
-                         npt, partials, rowlist, Mh);
-    else
-      hipLaunchKernelGGL(gemm_stats_f32_rows_kernel, grid, block, 0, stream, h, w, M, d, V, nvt,
-                         npt, partials, rowlist, Mh);
-  } else {
-    if (bf16)
-      hipLaunchKernelGGL(gemm_stats_bf16_kernel, grid, block, 0, stream, h, w, M, d, V, nvt, npt,
-                         partials);
-    else
-      hipLaunchKernelGGL(gemm_stats_f32_kernel, grid, block, 0, stream, h, w, M, d, V, nvt, npt,
-                         partials);
-  }
+  const bool draw = sample.row != nullptr;
+#define FORK_LAUNCH(K, ...) hipLaunchKernelGGL(K, grid, block, 0, stream, h, w, M, d, V, nvt, npt, \
+                                               partials, ##__VA_ARGS__)
+  if (bf16 && rowlist && draw)
+    FORK_LAUNCH(gemm_stats_bf16_rows_draw_kernel, rowlist, Mh, sample);
+  else if (bf16 && rowlist)
+    FORK_LAUNCH(gemm_stats_bf16_rows_kernel, rowlist, Mh);
+  else if (bf16 && draw)
+    FORK_LAUNCH(gemm_stats_bf16_draw_kernel, sample);
+  else if (bf16)
+    FORK_LAUNCH(gemm_stats_bf16_kernel);
+  else if (rowlist && draw)
+    FORK_LAUNCH(gemm_stats_f32_rows_draw_kernel, rowlist, Mh, sample);
+  else if (rowlist)
+    FORK_LAUNCH(gemm_stats_f32_rows_kernel, rowlist, Mh);
+  else if (draw)
+    FORK_LAUNCH(gemm_stats_f32_draw_kernel, sample);
+  else
+    FORK_LAUNCH(gemm_stats_f32_kernel);
+#undef FORK_LAUNCH
   return hipGetLastError();
 }
 

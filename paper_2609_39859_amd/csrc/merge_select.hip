@@ -9,7 +9,10 @@
 //   log-normaliser = m + log s,  entropy = -sum q log q = log s - t/s,
 // the quantities of Section 2 (confidence), Section 3.1 (entropy) and
 // Section 3.2 (log-probability inside the ForkGRPO ratio) of the Fork-dLLM
-// paper.  The merge order is fixed, so results are bit-reproducible.
+// paper.  For a drawn candidate x (sampling temperature > 0) the confidence
+// and log-probability are those of x under the untempered q: e^(z_x - m)/s
+// and (z_x - m) - log s.  The merge order is fixed, so results are
+// bit-reproducible.
 //
 // Selection (Algorithm 2 of the paper, in the active block of the
 // semi-autoregressive regime of Section 4.1): one wave64 per sequence; the
@@ -44,11 +47,20 @@ __device__ __forceinline__ float4 merge2(float4 a, float4 b) {
   return r;
 }
 
+// Drawn-candidate partials {key, idx bits, z, 0}: larger key wins, lower
+// index on equal keys.
+__device__ __forceinline__ float4 pick_drawn(float4 a, float4 b) {
+  const bool take_a = a.x > b.x || (a.x == b.x && __float_as_int(a.y) < __float_as_int(b.y));
+  return make_float4(take_a ? a.x : b.x, take_a ? a.y : b.y, take_a ? a.z : b.z, 0.f);
+}
+
 __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
     const float4* __restrict__ partials, int M, int nvt, float* __restrict__ conf,
     float* __restrict__ entropy, float* __restrict__ logp, float* __restrict__ lse,
-    int32_t* __restrict__ argmax, const int32_t* __restrict__ rowlist) {
+    int32_t* __restrict__ argmax, const int32_t* __restrict__ rowlist,
+    const int32_t* __restrict__ sample_row, const float4* __restrict__ spartials) {
   __shared__ float4 red[kMergeWaves][kMergeRows];
+  __shared__ float4 sred[kMergeWaves][kMergeRows];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int r = blockIdx.x * kMergeRows + lane;
@@ -57,17 +69,34 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
     for (int j = w; j < nvt; j += kMergeWaves)
       acc = merge2(acc, partials[(size_t)j * M + r]);
   red[w][lane] = acc;
+  // drawn candidate (positions marked in sample_row)
+  const bool drawn = sample_row && r < M && sample_row[r] >= 0;
+  float4 sacc = make_float4(-INFINITY, __int_as_float(0x7fffffff), 0.f, 0.f);
+  if (drawn)
+    for (int j = w; j < nvt; j += kMergeWaves)
+      sacc = pick_drawn(sacc, spartials[(size_t)j * M + r]);
+  sred[w][lane] = sacc;
   __syncthreads();
   const int dst = r < M ? (rowlist ? rowlist[r] : r) : -1;
   if (w == 0 && dst >= 0) {
 #pragma unroll
     for (int k = 1; k < kMergeWaves; ++k) acc = merge2(acc, red[k][lane]);
     const float log_s = logf(acc.y);
-    conf[dst] = 1.0f / acc.y;
-    logp[dst] = -log_s;
     entropy[dst] = log_s - acc.z / acc.y;
     if (lse) lse[dst] = acc.x + log_s;
-    argmax[dst] = __float_as_int(acc.w);
+    if (drawn) {
+#pragma unroll
+      for (int k = 1; k < kMergeWaves; ++k) sacc = pick_drawn(sacc, sred[k][lane]);
+      // untempered q of the drawn token: exp(z - m) / s
+      const float dz = sacc.z - acc.x;
+      conf[dst] = exp2f(dz * kLog2e) / acc.y;
+      logp[dst] = dz - log_s;
+      argmax[dst] = __float_as_int(sacc.y);
+    } else {
+      conf[dst] = 1.0f / acc.y;
+      logp[dst] = -log_s;
+      argmax[dst] = __float_as_int(acc.w);
+    }
   }
 }
 
@@ -220,7 +249,8 @@ __global__ __launch_bounds__(64) void select_kernel(
 __global__ __launch_bounds__(64) void active_rows_kernel(int L, int BL,
                                                         const uint8_t* __restrict__ mask,
                                                         const int32_t* __restrict__ block_start,
-                                                        int32_t* __restrict__ rowlist) {
+                                                        int32_t* __restrict__ rowlist,
+                                                        int32_t* __restrict__ rowmap) {
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const size_t base = (size_t)b * L;
@@ -241,27 +271,32 @@ __global__ __launch_bounds__(64) void active_rows_kernel(int L, int BL,
     }
   }
   const int e = found ? min(s + BL, L) : 0;
-  for (int i = lane; i < BL; i += 64)
-    rowlist[(size_t)b * BL + i] = (found && s + i < e) ? (int32_t)(base + s + i) : -1;
+  if (rowlist)
+    for (int i = lane; i < BL; i += 64)
+      rowlist[(size_t)b * BL + i] = (found && s + i < e) ? (int32_t)(base + s + i) : -1;
+  if (rowmap)
+    for (int k = lane; k < L; k += 64)
+      rowmap[base + k] = (found && k >= s && k < e) ? (int32_t)(base + k) : -1;
 }
 
 }  // namespace
 
 hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
-                              const int32_t* block_start, int32_t* rowlist,
+                              const int32_t* block_start, int32_t* rowlist, int32_t* rowmap,
                               hipStream_t stream) {
   hipLaunchKernelGGL(active_rows_kernel, dim3((unsigned)B), dim3(64), 0, stream, L, block_len,
-                     mask, block_start, rowlist);
+                     mask, block_start, rowlist, rowmap);
   return hipGetLastError();
 }
 
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse, int32_t* argmax,
-                        const int32_t* rowlist, hipStream_t stream) {
+                        const int32_t* rowlist, const int32_t* sample_row,
+                        const float4* spartials, hipStream_t stream) {
   const dim3 grid((unsigned)((M + kMergeRows - 1) / kMergeRows));
   const dim3 block(kMergeRows * kMergeWaves);
   hipLaunchKernelGGL(merge_kernel, grid, block, 0, stream, partials, M, nvt, conf,
-                     entropy, logp, lse, argmax, rowlist);
+                     entropy, logp, lse, argmax, rowlist, sample_row, spartials);
   return hipGetLastError();
 }
 

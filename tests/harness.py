@@ -53,7 +53,7 @@ class GpuOut:
 
 def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
              rule=_binding.FORK_RULE_LEFTMOST, workspace=None, uniform=None,
-             rows_mode=_binding.FORK_ROWS_ALL) -> GpuOut:
+             rows_mode=_binding.FORK_ROWS_ALL, temperature=0.0, seed=0, counter=0) -> GpuOut:
     """One step through fork_step_ex on the device of h_dev; host inputs for
     the state, host copies of every output.  Per-position outputs start as
     NaN (statistics) and -7 (candidates), so rows a step leaves untouched are
@@ -74,7 +74,8 @@ def gpu_step(h_dev, W_dev, tokens, mask, block_start, B, L, block_len, tau,
     _binding.fork_step_ex(h_dev, W_dev, tok, msk, bs, block_len, tau, conf, ent, logp, fb,
                           B=B, L=L, out_lse=lse, out_argmax=am, out_ncommit=nc,
                           out_commit_pos=cp, rule=rule, workspace=workspace,
-                          fallback_uniform=uni, rows_mode=rows_mode)
+                          fallback_uniform=uni, rows_mode=rows_mode,
+                          temperature=temperature, seed=seed, counter=counter)
     torch.cuda.synchronize(dev)
     c = lambda t: t.cpu().numpy()
     return GpuOut(c(conf), c(ent), c(logp), c(lse), c(am), c(tok), c(msk), c(bs), c(fb),
@@ -122,6 +123,59 @@ def compare_stats(g: GpuOut, ref: dict, rows, hbits, Wbits, d: int, rep: Report)
         zmax = exact_logit(hbits, Wbits, r, int(ref["argmax"][i]))
         zg = exact_logit(hbits, Wbits, r, int(ga[i]))
         assert zmax - zg <= gt, "row %d: candidate %d is not a maximiser" % (r, ga[i])
+    rep.rows += rows.size
+    rep.near_tie_rows += int(mism.size)
+    return rows[mism]
+
+
+def key_tol(d: int, temperature: float) -> float:
+    """Two Gumbel keys closer than this may be ordered either way: the logit
+    error (GAP_TOL) scaled by 1/temperature, plus binary32 rounding of the
+    perturbation (|log E| < 17, relative error ~1e-7)."""
+    return gap_tol(d) / temperature + 1e-4
+
+
+def oracle_key(hbits, Wbits, r, v, temperature, seed, counter) -> float:
+    """The oracle's Gumbel key of vocabulary entry v at row r."""
+    e, _ = oracle.exp_draw(seed, counter, r, v)
+    return exact_logit(hbits, Wbits, r, v) / temperature - float(np.log(e))
+
+
+def compare_sampled(g: GpuOut, st: dict, sm: dict, rows, hbits, Wbits, d: int,
+                    temperature: float, seed: int, counter: int, rep: Report):
+    """Rows whose candidates are drawn: entropy and log-normaliser against
+    the oracle's statistics `st`; the drawn token against the oracle's draw
+    `sm` (identical, or both within key_tol of the best key when the
+    oracle's top-2 key gap is below it); confidence and log-probability
+    against the oracle's untempered q of the GPU's token.  Returns the rows
+    whose token differs."""
+    rows = np.asarray(rows)
+    for k in ("entropy", "lse"):
+        gv = getattr(g, k)[rows].astype(np.float64)
+        err = np.abs(gv - st[k])
+        if k == "lse":
+            err = err / np.maximum(1.0, np.abs(st[k]))
+        rep.max_err[k] = max(rep.max_err.get(k, 0.0), float(err.max()) if err.size else 0.0)
+        assert np.all(err <= STAT_TOL), "%s off on drawn rows (max %g)" % (k, err.max())
+    kt = key_tol(d, temperature)
+    ga = g.argmax[rows]
+    logq = sm["logp"].copy()
+    mism = np.nonzero(ga != sm["cand"])[0]
+    for i in mism:
+        r = int(rows[i])
+        assert sm["keygap"][i] < kt, "row %d: drawn %d vs oracle %d (key gap %g)" % (
+            r, ga[i], sm["cand"][i], sm["keygap"][i])
+        kbest = oracle_key(hbits, Wbits, r, int(sm["cand"][i]), temperature, seed, counter)
+        kg = oracle_key(hbits, Wbits, r, int(ga[i]), temperature, seed, counter)
+        assert kbest - kg <= kt, "row %d: drawn %d is not a maximiser of the keys" % (r, ga[i])
+        logq[i] = exact_logit(hbits, Wbits, r, int(ga[i])) - st["lse"][i]
+    for k, ref in (("conf", np.exp(logq)), ("logp", logq)):
+        gv = getattr(g, k)[rows].astype(np.float64)
+        err = np.abs(gv - ref)
+        rep.max_err[k] = max(rep.max_err.get(k, 0.0), float(err.max()) if err.size else 0.0)
+        bad = np.nonzero(~(err <= STAT_TOL))[0]
+        assert bad.size == 0, "%s: %d drawn rows off, e.g. row %d gpu %r oracle %r" % (
+            k, bad.size, rows[bad[0]], gv[bad[0]], ref[bad[0]])
     rep.rows += rows.size
     rep.near_tie_rows += int(mism.size)
     return rows[mism]
@@ -176,8 +230,11 @@ KEY_TIE_TOL = {2: 1e-5, 3: 1e-4}
 
 def compare_decisions(g: GpuOut, sel, conf_ref, tokens, mask, block_start, B, L, BL,
                       tau, rep: Report, seqs=None, rule=0, near_tie_rows=(),
-                      entropy_ref=None, uniform=None):
-    """sel = oracle select output on oracle confidences and candidates."""
+                      entropy_ref=None, uniform=None, tie_seqs_excluded=False):
+    """sel = oracle select output on oracle confidences and candidates.
+    With tie_seqs_excluded, a sequence whose active block holds a near-tie
+    row is excluded too (a drawn token that differs carries a different
+    confidence, so the threshold decision may legitimately differ)."""
     tok_o, msk_o, bs_o, fb_o, nc_o = sel
     lam = float(np.float32(tau))
     seqs = list(range(B) if seqs is None else seqs)
@@ -199,6 +256,8 @@ def compare_decisions(g: GpuOut, sel, conf_ref, tokens, mask, block_start, B, L,
                 srt = np.sort(key)
                 gap = srt[1] - srt[0] if rule == 2 else srt[-1] - srt[-2]
                 near = near or gap < KEY_TIE_TOL[rule]
+        if tie_seqs_excluded and fb_o[b] != -1:
+            near = near or any(b * L + k in tie for k in range(s, min(s + BL, L)))
         if near:
             rep.near_threshold_seqs += 1
             continue

@@ -43,11 +43,12 @@ def test_version_and_workspace_sizes():
     assert L.fork_version() == 10000
     # per-tile partials (16 B per position per 256-entry vocabulary tile,
     # padded to 256 B) + candidates and active-row list (4 B per position each)
+    # + the per-tile drawn candidates (as large as the partials)
     def expect(B, Lq, V):
         M = B * Lq
         nvt = (V + 255) // 256
         pad = lambda x: (x + 255) // 256 * 256
-        return pad(nvt * M * 16) + pad(M * 4) + pad(M * 4)
+        return 2 * pad(nvt * M * 16) + pad(M * 4) + pad(M * 4)
     for B, Lq, V in [(1, 64, 1024), (4, 256, 32000), (8, 512, 126464), (3, 37, 1013)]:
         assert L.fork_workspace_bytes(B, Lq, V) == expect(B, Lq, V)
     assert L.fork_workspace_bytes(0, 5, 5) == 0
@@ -79,6 +80,9 @@ def _args(**kw):
     (dict(rule=5), _binding.FORK_EINVAL),
     (dict(rule=-1), _binding.FORK_EINVAL),
     (dict(rows_mode=2), _binding.FORK_EINVAL),
+    (dict(sample_temperature=-0.5), _binding.FORK_EINVAL),
+    (dict(sample_temperature=float("nan")), _binding.FORK_EINVAL),
+    (dict(sample_temperature=float("inf")), _binding.FORK_EINVAL),
     (dict(rows_mode=1, B=64, L=2048, d=8192), _binding.FORK_EUNSUPPORTED),
     (dict(rule=4), _binding.FORK_EINVAL),          # random rule without uniforms
     (dict(d=12), _binding.FORK_EUNSUPPORTED),
