@@ -21,6 +21,11 @@ Algorithm 2, Algorithm 1 for the differential tests, Section 3.2):
   x_0^k ~ q(. | x_t; tau) of Section 2, by the Gumbel-max property with
   Philox4x32-10 draws), with the untempered q and log q of the drawn token;
   ``philox``, ``exp_draw`` expose the generator.
+* ``token_logprob``, ``grpo_objective``, ``top_entropy`` -- the ForkGRPO
+  side of Section 3.2: teacher-forced log-probabilities of given tokens, the
+  clipped surrogate averaged over each rollout's fallback steps with
+  group-normalised advantages, and JustGRPO-Fast's highest-entropy
+  positions.
 """
 from __future__ import annotations
 
@@ -98,7 +103,78 @@ class Oracle:
                                           ctypes.c_int64, P, ctypes.c_int64,
                                           ctypes.c_double, ctypes.c_uint64, ctypes.c_uint32,
                                           P, P, P, P, ctypes.c_int]
+        lib.oracle_token_logprob.restype = ctypes.c_int
+        lib.oracle_token_logprob.argtypes = [P, P, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                             ctypes.c_int64, P, P, ctypes.c_int64, P, P,
+                                             ctypes.c_int]
+        lib.oracle_grpo_objective.restype = ctypes.c_int
+        lib.oracle_grpo_objective.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P,
+                                              ctypes.c_double, P, P, P, P, P, P, P]
+        lib.oracle_top_entropy.restype = ctypes.c_int
+        lib.oracle_top_entropy.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P]
         self.lib = lib
+
+    def token_logprob(self, hidden, W, rows, tokens, nthreads: int = 0):
+        """log q(tokens[e]) and the entropy at hidden row rows[e]."""
+        h, dt_h = _as_input(hidden)
+        w, dt_w = _as_input(W)
+        if dt_h != dt_w:
+            raise TypeError("hidden and W must share a dtype")
+        M, d = h.shape
+        V, d2 = w.shape
+        if d != d2:
+            raise ValueError("hidden is [M, %d] but W is [V, %d]" % (d, d2))
+        rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64)).reshape(-1)
+        tokens = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32)).reshape(-1)
+        if rows.size != tokens.size:
+            raise ValueError("rows and tokens differ in length")
+        n = rows.size
+        logp = np.empty(n, np.float64)
+        ent = np.empty(n, np.float64)
+        rc = self.lib.oracle_token_logprob(_ptr(h), _ptr(w), dt_h, M, d, V, _ptr(rows),
+                                           _ptr(tokens), n, _ptr(logp), _ptr(ent), int(nthreads))
+        if rc == -2:
+            raise FloatingPointError("non-finite logit")
+        if rc != 0:
+            raise ValueError("oracle_token_logprob rejected its arguments (%d)" % rc)
+        return {"logp": logp, "entropy": ent}
+
+    def grpo_objective(self, rewards, offsets, lp_new, lp_old, G, eps):
+        """ForkGRPO objective; rewards [n_groups * G], offsets [n_groups * G + 1]."""
+        rewards = np.ascontiguousarray(rewards, dtype=np.float64).reshape(-1)
+        offsets = np.ascontiguousarray(offsets, dtype=np.int32).reshape(-1)
+        lp_new = np.ascontiguousarray(lp_new, dtype=np.float64).reshape(-1)
+        lp_old = np.ascontiguousarray(lp_old, dtype=np.float64).reshape(-1)
+        R = rewards.size
+        if R % G or offsets.size != R + 1:
+            raise ValueError("rewards must hold n_groups * G entries and offsets one more")
+        ng = R // G
+        n = lp_new.size
+        out = {"adv": np.empty(R), "ratio": np.empty(n), "term": np.empty(n),
+               "rollout_obj": np.empty(R), "group_obj": np.empty(ng),
+               "skipped": np.empty(ng, np.uint8)}
+        J = ctypes.c_double()
+        rc = self.lib.oracle_grpo_objective(ng, int(G), _ptr(rewards), _ptr(offsets),
+                                            _ptr(lp_new), _ptr(lp_old), float(eps),
+                                            _ptr(out["adv"]), _ptr(out["ratio"]), _ptr(out["term"]),
+                                            _ptr(out["rollout_obj"]), _ptr(out["group_obj"]),
+                                            _ptr(out["skipped"]), ctypes.byref(J))
+        if rc != 0:
+            raise ValueError("oracle_grpo_objective rejected its arguments (%d)" % rc)
+        out["J"] = J.value
+        return out
+
+    def top_entropy(self, entropy, k):
+        """[R, Lg] entropies -> [R, Lg] uint8 selection of the k highest per row."""
+        ent = np.ascontiguousarray(entropy, dtype=np.float64)
+        if ent.ndim != 2:
+            raise ValueError("entropy must be [R, Lg]")
+        R, Lg = ent.shape
+        sel = np.empty((R, Lg), np.uint8)
+        rc = self.lib.oracle_top_entropy(R, Lg, int(k), _ptr(ent), _ptr(sel))
+        if rc != 0:
+            raise ValueError("oracle_top_entropy rejected its arguments (%d)" % rc)
+        return sel
 
     def philox(self, ctr, key):
         """Philox4x32-10 of a 4-word counter under a 2-word key."""
@@ -266,6 +342,18 @@ def row_sample(*a, **k):
 
 def philox(*a, **k):
     return default().philox(*a, **k)
+
+
+def token_logprob(*a, **k):
+    return default().token_logprob(*a, **k)
+
+
+def grpo_objective(*a, **k):
+    return default().grpo_objective(*a, **k)
+
+
+def top_entropy(*a, **k):
+    return default().top_entropy(*a, **k)
 
 
 def exp_draw(*a, **k):

@@ -54,6 +54,16 @@ static double log_normaliser(const double* z, int64_t V) {
   return zmax + log(sum);
 }
 
+/* entropy -sum_v q_v log q_v with log q_v = z_v - log_norm (Section 3.1) */
+static double entropy_of(const double* z, int64_t V, double log_norm) {
+  double h = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    double lq = z[v] - log_norm;
+    h -= exp(lq) * lq;
+  }
+  return h;
+}
+
 /* Statistics of q(. | x_t) for one position, from the definitions in Section 2
  * (the model's per-position categorical, the greedy candidate and its
  * confidence) and Section 3.1 (token entropy).  Returns 0, or -2 when a logit
@@ -70,12 +80,7 @@ static int one_row(const void* hidden, const void* W, int dtype, int64_t d,
     if (z[v] > z[a]) a = v;
   double zmax = z[a];
   double log_norm = log_normaliser(z, V);
-  /* entropy -sum q log q with log q_v = z_v - log_norm */
-  double h = 0.0;
-  for (int64_t v = 0; v < V; ++v) {
-    double lq = z[v] - log_norm;
-    h -= exp(lq) * lq;
-  }
+  double h = entropy_of(z, V, log_norm);
   /* gap to the runner-up (any index other than a) */
   double second = -INFINITY;
   for (int64_t v = 0; v < V; ++v)
@@ -355,4 +360,126 @@ int oracle_select(int32_t B, int32_t L, int32_t block_len, const double* conf,
   if (rule != ORACLE_RULE_LEFTMOST && rule != ORACLE_RULE_MAXCONF) return -1;
   return oracle_select_ex(B, L, block_len, conf, NULL, NULL, argmax_tok, lambda,
                           rule, tokens, mask, block_start, fallback, ncommit);
+}
+
+/* ------------------------------------------------------------ ForkGRPO */
+
+int oracle_token_logprob(const void* hidden, const void* W, int dtype,
+                         int64_t M, int64_t d, int64_t V, const int64_t* rows,
+                         const int32_t* tokens, int64_t n, double* logp,
+                         double* entropy, int nthreads) {
+  if (!hidden || !W || (n > 0 && (!rows || !tokens || !logp)) || M <= 0 || d <= 0 ||
+      V <= 0 || V > INT32_MAX || n < 0)
+    return -1;
+  if (dtype != ORACLE_BF16 && dtype != ORACLE_F32) return -1;
+  for (int64_t e = 0; e < n; ++e)
+    if (rows[e] < 0 || rows[e] >= M || tokens[e] < 0 || tokens[e] >= V) return -1;
+  int status = 0;
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#pragma omp parallel num_threads(nthreads)
+#endif
+  {
+    double* z = (double*)malloc((size_t)V * sizeof(double));
+    if (!z) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      status = -1;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t e = 0; e < n; ++e) {
+        int rc = logits(hidden, W, dtype, d, V, rows[e], z);
+        if (rc) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+          status = rc;
+          continue;
+        }
+        const double log_norm = log_normaliser(z, V);
+        /* log q of the given token: its logit against the normaliser */
+        logp[e] = z[tokens[e]] - log_norm;
+        if (entropy) entropy[e] = entropy_of(z, V, log_norm);
+      }
+      free(z);
+    }
+  }
+  (void)nthreads;
+  return status;
+}
+
+int oracle_grpo_objective(int32_t n_groups, int32_t G, const double* rewards,
+                          const int32_t* offsets, const double* lp_new,
+                          const double* lp_old, double eps, double* adv,
+                          double* ratio, double* term, double* rollout_obj,
+                          double* group_obj, uint8_t* skipped, double* J) {
+  if (n_groups < 0 || G <= 0 || !rewards || !offsets || !(eps >= 0.0)) return -1;
+  const int64_t R = (int64_t)n_groups * G;
+  if (offsets[0] != 0) return -1;
+  for (int64_t i = 0; i < R; ++i)
+    if (offsets[i + 1] < offsets[i]) return -1;
+  if (offsets[R] > 0 && (!lp_new || !lp_old)) return -1;
+  double total = 0.0;
+  int32_t kept = 0;
+  for (int32_t g = 0; g < n_groups; ++g) {
+    const double* r = rewards + (int64_t)g * G;
+    /* group mean and standard deviation (divisor G) of the rewards */
+    double mean = 0.0;
+    for (int32_t j = 0; j < G; ++j) mean += r[j];
+    mean /= G;
+    double var = 0.0;
+    for (int32_t j = 0; j < G; ++j) var += (r[j] - mean) * (r[j] - mean);
+    const double sd = sqrt(var / G);
+    const int skip = !(sd > 0.0);
+    double gsum = 0.0;
+    for (int32_t j = 0; j < G; ++j) {
+      const int64_t i = (int64_t)g * G + j;
+      const double A = skip ? 0.0 : (r[j] - mean) / sd;
+      if (adv) adv[i] = A;
+      double acc = 0.0;
+      const int32_t nF = offsets[i + 1] - offsets[i];
+      for (int32_t e = offsets[i]; e < offsets[i + 1]; ++e) {
+        const double rho = exp(lp_new[e] - lp_old[e]);
+        const double clipped = rho < 1.0 - eps ? 1.0 - eps : (rho > 1.0 + eps ? 1.0 + eps : rho);
+        const double a = rho * A, b = clipped * A;
+        const double tm = a < b ? a : b;
+        if (ratio) ratio[e] = rho;
+        if (term) term[e] = tm;
+        acc += tm;
+      }
+      const double ro = nF > 0 ? acc / nF : 0.0;
+      if (rollout_obj) rollout_obj[i] = ro;
+      gsum += ro;
+    }
+    const double go = skip ? 0.0 : gsum / G;
+    if (group_obj) group_obj[g] = go;
+    if (skipped) skipped[g] = (uint8_t)skip;
+    if (!skip) {
+      total += go;
+      ++kept;
+    }
+  }
+  if (J) *J = kept > 0 ? total / kept : 0.0;
+  return 0;
+}
+
+int oracle_top_entropy(int32_t R, int32_t Lg, int32_t k, const double* entropy,
+                       uint8_t* sel) {
+  if (R < 0 || Lg <= 0 || k < 0 || k > Lg || (R > 0 && (!entropy || !sel))) return -1;
+  for (int32_t i = 0; i < R; ++i) {
+    const double* h = entropy + (int64_t)i * Lg;
+    uint8_t* out = sel + (int64_t)i * Lg;
+    /* a position is chosen when fewer than k positions come before it in
+       the order (higher entropy first, then lower position) */
+    for (int32_t p = 0; p < Lg; ++p) {
+      int32_t ahead = 0;
+      for (int32_t q = 0; q < Lg; ++q)
+        if (h[q] > h[p] || (h[q] == h[p] && q < p)) ++ahead;
+      out[p] = (uint8_t)(ahead < k);
+    }
+  }
+  return 0;
 }

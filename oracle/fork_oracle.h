@@ -134,6 +134,51 @@ int oracle_row_sample(const void* hidden, const void* W, int dtype,
                       int32_t* cand, double* conf, double* logp,
                       double* keygap, int nthreads);
 
+/*
+ * Teacher-forced log-probabilities (the numerator and denominator of the
+ * ForkGRPO ratio, Section 3.2): for each entry e, with z the logits of
+ * hidden row rows[e],
+ *   logp[e]    = z_{tokens[e]} - log sum_v exp(z_v)
+ *   entropy[e] = -sum_v q_v log q_v            (may be NULL)
+ * Returns 0, -1 on bad arguments (a row outside [0, M) or a token outside
+ * [0, V) included), -2 if a logit is not finite.
+ */
+int oracle_token_logprob(const void* hidden, const void* W, int dtype,
+                         int64_t M, int64_t d, int64_t V,
+                         const int64_t* rows, const int32_t* tokens, int64_t n,
+                         double* logp, double* entropy, int nthreads);
+
+/*
+ * The ForkGRPO objective of Section 3.2 on one batch of n_groups prompts
+ * with G rollouts each (rollout i = g * G + j).  Entries e of rollout i
+ * (its fallback steps t in F_i) are [offsets[i], offsets[i+1]).
+ *   A_i          = (r_i - mean_g) / std_g     (group-normalised advantage;
+ *                  std over the G rewards of the group, divisor G)
+ *   groups with std_g == 0 are skipped: their A_i = 0 and they are left out
+ *   of the mean below (group_obj = 0, skipped[g] = 1)
+ *   ratio[e]     = exp(lp_new[e] - lp_old[e])
+ *   term[e]      = min(ratio * A_i, clip(ratio, 1 - eps, 1 + eps) * A_i)
+ *   rollout_obj  = (1 / |F_i|) sum_{e in F_i} term[e]    (0 if F_i is empty)
+ *   group_obj[g] = (1 / G) sum_{i in g} rollout_obj[i]
+ *   *J           = mean of group_obj over the groups not skipped (0 if none)
+ * Any output array may be NULL.  Returns 0, or -1 on bad arguments.
+ */
+int oracle_grpo_objective(int32_t n_groups, int32_t G, const double* rewards,
+                          const int32_t* offsets, const double* lp_new,
+                          const double* lp_old, double eps, double* adv,
+                          double* ratio, double* term, double* rollout_obj,
+                          double* group_obj, uint8_t* skipped, double* J);
+
+/*
+ * JustGRPO-Fast position selection (Section 3.2): in each of R rollouts of
+ * Lg positions, the k positions of highest entropy (entropy[i * Lg + p]);
+ * equal entropies are taken in increasing position.  sel[i * Lg + p] = 1 for
+ * the chosen positions, 0 otherwise.  Returns 0, or -1 on bad arguments
+ * (k outside [0, Lg] included).
+ */
+int oracle_top_entropy(int32_t R, int32_t Lg, int32_t k, const double* entropy,
+                       uint8_t* sel);
+
 #ifdef __cplusplus
 }
 #endif

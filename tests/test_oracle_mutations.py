@@ -23,7 +23,7 @@ MUTATIONS = {
     "transposed_weight": ("widen(W, dtype, v * d + j)", "widen(W, dtype, j * V + v)"),
     "no_max_shift": ("sum += exp(z[v] - zmax);", "sum += exp(z[v]);"),
     "entropy_sign": ("h -= exp(lq) * lq;", "h += exp(lq) * lq;"),
-    "entropy_drops_norm": ("double lq = z[v] - log_norm;", "double lq = z[v] - zmax;"),
+    "entropy_drops_norm": ("double lq = z[v] - log_norm;", "double lq = z[v] - z[0];"),
     "logp_drops_logit": ("*logp = z[a] - log_norm;", "*logp = -log_norm;"),
     "conf_unnormalised": ("*conf = exp(z[a] - log_norm);", "*conf = exp(z[a] - zmax);"),
     "threshold_not_strict": ("conf[base + k] > lambda", "conf[base + k] >= lambda"),
@@ -50,6 +50,15 @@ MUTATIONS = {
     "sample_logq_drops_logit": ("const double log_q = z[a] - log_norm;",
                               "const double log_q = log_norm - log_norm;"),
     "keygap_stale_second": ("      second = best;\n      best = key;", "      best = key;"),
+    "logprob_wrong_index": ("logp[e] = z[tokens[e]] - log_norm;", "logp[e] = z[e] - log_norm;"),
+    "grpo_std_divisor": ("sqrt(var / G)", "sqrt(var / (G - 1))"),
+    "grpo_max_not_min": ("const double tm = a < b ? a : b;", "const double tm = a > b ? a : b;"),
+    "grpo_clip_lower_bound": ("rho < 1.0 - eps ? 1.0 - eps", "rho < 1.0 - eps ? 1.0 + eps"),
+    "grpo_no_skip": ("const int skip = !(sd > 0.0);", "const int skip = 0;"),
+    "grpo_rollout_sum": ("nF > 0 ? acc / nF : 0.0", "nF > 0 ? acc : 0.0"),
+    "grpo_mean_over_all_groups": ("kept > 0 ? total / kept : 0.0", "n_groups > 0 ? total / n_groups : 0.0"),
+    "top_entropy_tie_highest": ("(h[q] == h[p] && q < p)", "(h[q] == h[p] && q > p)"),
+    "top_entropy_lowest": ("if (h[q] > h[p] ||", "if (h[q] < h[p] ||"),
 }
 
 
@@ -76,6 +85,11 @@ def _checks(orc):
         lambda: pins.test_sample_frequencies_follow_tempered_softmax(orc, 0.5),
         lambda: pins.test_sample_low_temperature_is_greedy(orc),
         lambda: pins.test_sample_brute_force_keys(orc),
+        lambda: pins.test_token_logprob_brute_force(orc),
+        lambda: pins.test_grpo_hand_worked_fixture(orc),
+        lambda: pins.test_grpo_invariants(orc, 0),
+        lambda: pins.test_top_entropy_hand_worked(orc),
+        lambda: pins.test_top_entropy_matches_sort(orc, 52),
     ]
     failed = 0
     for c in calls:

@@ -522,3 +522,135 @@ def test_sample_rejects_bad_temperature(orc, tau):
     h = np.ones((1, 4), np.float32)
     with pytest.raises(ValueError):
         orc.row_sample(h, h, None, tau, seed=0, counter=0)
+
+
+# ------------------------------------------------------------------ ForkGRPO
+
+def test_token_logprob_brute_force(orc):
+    """log q of given tokens against scipy's log_softmax of numpy logits,
+    entropies against scipy's entropy; rows repeated and out of order."""
+    rng = np.random.default_rng(21)
+    for dtype in ("f32", "bf16"):
+        h = rng.standard_normal((9, 40)).astype(np.float32) * 2
+        W = rng.standard_normal((300, 40)).astype(np.float32) / 4
+        if dtype == "bf16":
+            hb = torch.from_numpy(h).to(torch.bfloat16)
+            Wb = torch.from_numpy(W).to(torch.bfloat16)
+            h, W = synth.to_bits(hb), synth.to_bits(Wb)
+            h64, W64 = hb.double().numpy(), Wb.double().numpy()
+        else:
+            h64, W64 = h.astype(np.float64), W.astype(np.float64)
+        rows = np.array([3, 0, 8, 3, 5, 1])
+        toks = np.array([0, 299, 17, 150, 42, 42])
+        out = orc.token_logprob(h, W, rows, toks)
+        z = h64[rows] @ W64.T
+        ls = scipy.special.log_softmax(z, axis=1)
+        np.testing.assert_allclose(out["logp"], ls[np.arange(rows.size), toks], atol=1e-11)
+        np.testing.assert_allclose(out["entropy"], scipy.stats.entropy(np.exp(ls), axis=1),
+                                   atol=1e-11)
+
+
+def test_token_logprob_of_candidate_is_row_stats_logp(orc):
+    rng = np.random.default_rng(4)
+    h = rng.standard_normal((12, 64)).astype(np.float32)
+    W = rng.standard_normal((500, 64)).astype(np.float32)
+    st = orc.row_stats(h, W)
+    out = orc.token_logprob(h, W, np.arange(12), st["argmax"])
+    np.testing.assert_allclose(out["logp"], st["logp"], atol=1e-12)
+    np.testing.assert_allclose(out["entropy"], st["entropy"], atol=1e-12)
+
+
+@pytest.mark.parametrize("rows,toks", [([5], [0]), ([-1], [0]), ([0], [300]), ([0], [-1])])
+def test_token_logprob_rejects_out_of_range(orc, rows, toks):
+    h = np.ones((5, 8), np.float32)
+    W = np.ones((300, 8), np.float32)
+    with pytest.raises(ValueError):
+        orc.token_logprob(h, W, rows, toks)
+
+
+def _grpo_fixture():
+    with open(os.path.join(GOLDEN, "grpo_worked.json")) as f:
+        return json.load(f)
+
+
+def test_grpo_hand_worked_fixture(orc):
+    fx = _grpo_fixture()
+    lp_old = np.linspace(-3.0, -0.5, len(fx["ratios"]))
+    lp_new = lp_old + np.log(np.array(fx["ratios"], np.float64))
+    out = orc.grpo_objective(fx["rewards"], fx["offsets"], lp_new, lp_old, fx["G"], fx["eps"])
+    ex = fx["expected"]
+    for k in ("adv", "term", "rollout_obj", "group_obj"):
+        np.testing.assert_allclose(out[k], ex[k]["values"], atol=1e-12, err_msg=k)
+    assert out["skipped"].tolist() == ex["skipped"]
+    assert out["J"] == pytest.approx(ex["J"]["value"], abs=1e-14)
+    np.testing.assert_allclose(out["ratio"], fx["ratios"], rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_grpo_invariants(orc, seed):
+    """With the new policy equal to the old one (rho = 1) and every rollout
+    holding a fallback step, each term is A_i and the advantages of a group
+    sum to zero, so J = 0; an affine change of the rewards (positive scale)
+    leaves every advantage and J unchanged; eps = inf removes the clip."""
+    rng = np.random.default_rng(seed)
+    ng, G = 5, 16
+    R = ng * G
+    nF = rng.integers(1, 20, R)
+    off = np.concatenate([[0], np.cumsum(nF)]).astype(np.int32)
+    rewards = rng.integers(0, 2, R).astype(np.float64)
+    rewards[:G] = 1.0                              # one group with std 0
+    lp_old = -rng.random(off[-1]) * 5
+    out = orc.grpo_objective(rewards, off, lp_old, lp_old, G, 0.2)
+    assert out["J"] == pytest.approx(0.0, abs=1e-12)
+    assert out["skipped"][0] == 1 and np.all(out["adv"][:G] == 0)
+    lp_new = lp_old + rng.normal(0, 0.3, off[-1])
+    a = orc.grpo_objective(rewards, off, lp_new, lp_old, G, 0.2)
+    b = orc.grpo_objective(3.0 * rewards - 7.0, off, lp_new, lp_old, G, 0.2)
+    np.testing.assert_allclose(a["adv"], b["adv"], atol=1e-12)
+    assert a["J"] == pytest.approx(b["J"], abs=1e-12)
+    for g in range(ng):
+        if not a["skipped"][g]:
+            adv = a["adv"][g * G:(g + 1) * G]
+            assert abs(adv.sum()) < 1e-9 and abs((adv ** 2).mean() - 1.0) < 1e-9
+    c = orc.grpo_objective(rewards, off, lp_new, lp_old, G, float("inf"))
+    rho = np.exp(lp_new - lp_old)
+    A = np.repeat(c["adv"], nF)
+    np.testing.assert_allclose(c["term"], rho * A, rtol=1e-12)
+    # clipping only ever lowers the objective: min(rho A, clip(rho) A) <= rho A
+    assert np.all(a["term"] <= rho * A + 1e-12)
+
+
+def test_grpo_rejects_bad_arguments(orc):
+    with pytest.raises(ValueError):
+        orc.grpo_objective([1, 0], [0, 2, 1], [0, 0], [0, 0], 2, 0.2)   # decreasing offsets
+    with pytest.raises(ValueError):
+        orc.grpo_objective([1, 0], [0, 1, 2], [0, 0], [0, 0], 2, -0.1)  # eps < 0
+
+
+def test_top_entropy_hand_worked(orc):
+    ent = np.array([[0.5, 2.0, 2.0, 0.1, 1.0, 2.0],
+                    [1.0, 1.0, 1.0, 1.0, 1.0, 1.0]])
+    assert orc.top_entropy(ent, 2).tolist() == [[0, 1, 1, 0, 0, 0], [1, 1, 0, 0, 0, 0]]
+    assert orc.top_entropy(ent, 4).tolist() == [[0, 1, 1, 0, 1, 1], [1, 1, 1, 1, 0, 0]]
+    assert orc.top_entropy(ent, 0).sum() == 0 and orc.top_entropy(ent, 6).sum() == 12
+
+
+@pytest.mark.parametrize("k", [1, 52, 256])
+def test_top_entropy_matches_sort(orc, k):
+    """The selection is the first k positions of a stable sort by decreasing
+    entropy (numpy lexsort), with ties made frequent by rounding."""
+    rng = np.random.default_rng(k)
+    ent = np.round(rng.random((20, 256)) * 8, 1)
+    sel = orc.top_entropy(ent, k)
+    for i in range(ent.shape[0]):
+        order = np.lexsort((np.arange(256), -ent[i]))
+        expect = np.zeros(256, np.uint8)
+        expect[order[:k]] = 1
+        assert np.array_equal(sel[i], expect)
+
+
+def test_top_entropy_rejects_bad_k(orc):
+    with pytest.raises(ValueError):
+        orc.top_entropy(np.zeros((2, 5)), 6)
+    with pytest.raises(ValueError):
+        orc.top_entropy(np.zeros((2, 5)), -1)
