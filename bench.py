@@ -15,7 +15,9 @@ events recorded around that kernel alone on the stream it runs on.
 the same workload and scales it to steps per second.  `active_rows_mode`
 times the same decode with the LM head restricted to each sequence's active
 block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload; `drawn_candidates`
-times both modes with candidates drawn at sampling temperature 0.8.
+times both modes with candidates drawn at sampling temperature 0.8;
+`forkgrpo_likelihood` times one ForkGRPO batch of 4096 teacher-forced
+log-probabilities plus its objective.
 """
 import argparse
 import ctypes
@@ -96,6 +98,68 @@ def cpu_baseline(cfg, W_dev, h_dev, target_s):
                       % (rows.size, cfg.M, cfg.V, dt, threads, cfg.M)}
 
 
+def grpo_likelihood(args, hip, W, h, dev):
+    """One ForkGRPO likelihood batch: 16 prompts x 16 rollouts x 16 fallback
+    steps = 4096 teacher-forced entries (hidden rows [4096, d], given tokens)
+    through fork_logprob, then the clipped-surrogate objective over the
+    batch.  LM-head time from HIP events around its launch."""
+    import torch
+
+    from paper_2609_39859_amd import _binding
+    n_groups, G, per = 16, 16, 16
+    R = n_groups * G
+    n = R * per
+    V, d = W.shape
+    gen = torch.Generator(device=dev).manual_seed(0x6EED)
+    toks = torch.randint(0, V, (n,), generator=gen, device=dev, dtype=torch.int32)
+    hh = h[:n].contiguous()
+    lp_new, lp_old = (torch.empty(n, device=dev) for _ in range(2))
+    lp_old.copy_(-torch.rand(n, generator=gen, device=dev) * 8)
+    rewards = (torch.rand(R, generator=gen, device=dev) < 0.5).float()
+    offsets = torch.arange(0, n + 1, per, device=dev, dtype=torch.int32)
+    gobj = torch.empty(n_groups, device=dev)
+    skip = torch.empty(n_groups, dtype=torch.uint8, device=dev)
+    J = torch.empty(1, device=dev)
+    evs = []
+    for _ in range(2 * args.steps):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+        evs.append(e.value)
+
+    def batch(i=None):
+        _binding.logprob(hh, W, toks, lp_new,
+                         events=None if i is None else (evs[2 * i], evs[2 * i + 1]))
+        _binding.grpo_objective(rewards, offsets, lp_new, lp_old, G, 0.2, gobj, skip, J)
+
+    print("bench: timing %d ForkGRPO likelihood batches" % args.steps, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        batch()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.steps):
+        batch(i)
+    stop.record()
+    torch.cuda.synchronize()
+    assert math.isfinite(J.item())
+    lm = []
+    for i in range(args.steps):
+        ms = ctypes.c_float()
+        assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
+        lm.append(ms.value)
+    for e in evs:
+        hip.hipEventDestroy(e)
+    batch_ms = start.elapsed_time(stop) / args.steps
+    lm_ms = sum(lm) / len(lm)
+    tflops = 2.0 * n * d * V / (lm_ms * 1e-3) / 1e12
+    return {"entries": n, "groups": n_groups, "G": G, "fallback_steps_per_rollout": per,
+            "ms_per_batch": batch_ms, "lmhead_ms": lm_ms,
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
+                         "kernel": "gemm_stats_bf16_target_kernel (teacher-forced LM head)"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +172,8 @@ def main():
                     help="skip the extra timing of the active-block-only LM head")
     ap.add_argument("--no-drawn", action="store_true",
                     help="skip the extra timings with candidates drawn at temperature 0.8")
+    ap.add_argument("--no-grpo", action="store_true",
+                    help="skip the timing of the ForkGRPO likelihood batch")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -273,6 +339,8 @@ def main():
                             "steps_per_s": 1000.0 * args.steps / d_total,
                             "lmhead_ms": sum(d_lm) / len(d_lm), "kernel": kernel}
         out["drawn_candidates"] = drawn
+    if not args.no_grpo:
+        out["forkgrpo_likelihood"] = grpo_likelihood(args, hip, W, hs[0], dev)
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)

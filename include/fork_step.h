@@ -191,6 +191,90 @@ int fork_step_ex(const fork_step_args* args);
    are invalid. */
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
 
+/* ------------------------------------------------------------ ForkGRPO
+ *
+ * Section 3.2 of the paper trains on the fallback steps of Fork-dLLM
+ * rollouts: at each fallback step t of rollout i one token is committed at
+ * k_{i,t} (the leftmost masked position), so the policy-likelihood ratio
+ * rho_{i,t} = q_new(x^{k}|c, x_{i,t}) / q_old(x^{k}|c, x_{i,t}) is exact.
+ * fork_step records log q_old (out_logp at the committed position).  The
+ * calls below evaluate log q_new of the recorded tokens under another head
+ * (teacher forcing), the clipped surrogate objective, and JustGRPO-Fast's
+ * highest-entropy positions.
+ */
+
+/* Teacher-forced log-probabilities: for entry e, with z the logits of
+   hidden row rows[e] against W_head,
+     out_logp[e] = z_{tokens[e]} - log sum_v exp(z_v)     (log q of the token)
+   and optionally out_q[e] = exp(out_logp[e]), out_entropy[e] (nats) and
+   out_lse[e] = log sum_v exp(z_v).  A token outside [0, V) gives NaN; a row
+   outside [0, M) gives unspecified values (it is never read out of bounds).
+   Pointers are device pointers; the call is asynchronous on `stream`. */
+typedef struct fork_logprob_args {
+  const void* hidden;      /* [M, d], dtype                                    */
+  const void* W_head;      /* [V, d], dtype                                    */
+  const int32_t* rows;     /* [n] hidden row of each entry; NULL: row e        */
+  const int32_t* tokens;   /* [n] token of each entry                          */
+  float* out_logp;         /* [n]                                              */
+  float* out_q;            /* [n] or NULL                                      */
+  float* out_entropy;      /* [n] or NULL                                      */
+  float* out_lse;          /* [n] or NULL                                      */
+  int32_t n, M, d, V, dtype;
+  void* stream;
+  void* workspace;         /* NULL: library-managed, as for fork_step_ex       */
+  size_t workspace_bytes;
+  void* ev_lmhead_begin;   /* optional hipEvent_t pair around the LM head      */
+  void* ev_lmhead_end;
+} fork_logprob_args;
+
+/* FORK_OK, or FORK_EINVAL / FORK_EUNSUPPORTED (same size and alignment rules
+   as fork_step; with rows given, M*d*element_size < 2^31) / FORK_EHIP /
+   FORK_ENOMEM.  n == 0 enqueues nothing. */
+int fork_logprob(const fork_logprob_args* args);
+
+/* Workspace bytes of fork_logprob for n entries over V words. */
+size_t fork_logprob_workspace_bytes(int32_t n, int32_t V);
+
+/* The ForkGRPO objective (Section 3.2) of one batch: n_groups prompts with
+   G rollouts each, rollout i = g*G + j.  The fallback-step entries of
+   rollout i are [offsets[i], offsets[i+1]) of lp_new / lp_old (n entries).
+     A_i       = (r_i - mean_g) / std_g, std with divisor G; a group with
+                 std_g == 0 is skipped (A = 0, group_obj = 0, skipped = 1)
+     ratio[e]  = exp(lp_new[e] - lp_old[e])
+     term[e]   = min(ratio A_i, clip(ratio, 1 - eps, 1 + eps) A_i)
+     rollout_obj[i] = mean of term over the rollout's entries (0 if none)
+     group_obj[g]   = mean of rollout_obj over the group
+     J         = mean of group_obj over the groups not skipped (0 if none)
+   fp32 arithmetic, fixed-order sums (bit-reproducible).  Offsets are
+   clamped to [0, n].  Returns FORK_OK, FORK_EINVAL (sizes, G >
+   1024, eps < 0 or not finite, a required pointer NULL) or FORK_EHIP. */
+typedef struct fork_grpo_args {
+  int32_t n_groups, G, n;
+  const float* rewards;    /* [n_groups*G]                                     */
+  const int32_t* offsets;  /* [n_groups*G + 1]                                 */
+  const float* lp_new;     /* [n] log q under the policy being trained         */
+  const float* lp_old;     /* [n] log q recorded at rollout time               */
+  float eps;               /* clip range                                       */
+  float* out_adv;          /* [n_groups*G] or NULL                             */
+  float* out_ratio;        /* [n] or NULL                                      */
+  float* out_term;         /* [n] or NULL                                      */
+  float* out_rollout_obj;  /* [n_groups*G] or NULL                             */
+  float* out_group_obj;    /* [n_groups], required                             */
+  uint8_t* out_skipped;    /* [n_groups], required                             */
+  float* out_J;            /* [1], required                                    */
+  void* stream;
+} fork_grpo_args;
+int fork_grpo_objective(const fork_grpo_args* args);
+
+/* JustGRPO-Fast's position selection (compared with ForkGRPO in Section
+   3.2): in each of R rollouts of Lg positions (entropy[i*Lg + p], e.g. the
+   out_entropy recorded when position p was committed), sel[i*Lg + p] = 1
+   for the k positions of highest entropy, equal values taken in increasing
+   position, 0 elsewhere.  Lg <= 16384, 0 <= k <= Lg.  Returns FORK_OK,
+   FORK_EINVAL, FORK_EUNSUPPORTED (Lg too large) or FORK_EHIP. */
+int fork_top_entropy(const float* entropy, int32_t R, int32_t Lg, int32_t k, uint8_t* sel,
+                     void* stream);
+
 /* Description of the last non-OK return on the calling thread ("" if none).
    The string stays valid until the thread's next call into the library. */
 const char* fork_last_error(void);

@@ -53,6 +53,27 @@ class ForkStepArgs(ctypes.Structure):
     ]
 
 
+class ForkLogprobArgs(ctypes.Structure):
+    _fields_ = [
+        ("hidden", _P), ("W_head", _P), ("rows", _P), ("tokens", _P),
+        ("out_logp", _P), ("out_q", _P), ("out_entropy", _P), ("out_lse", _P),
+        ("n", _I32), ("M", _I32), ("d", _I32), ("V", _I32), ("dtype", _I32),
+        ("stream", _P), ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
+        ("ev_lmhead_begin", _P), ("ev_lmhead_end", _P),
+    ]
+
+
+class ForkGrpoArgs(ctypes.Structure):
+    _fields_ = [
+        ("n_groups", _I32), ("G", _I32), ("n", _I32),
+        ("rewards", _P), ("offsets", _P), ("lp_new", _P), ("lp_old", _P),
+        ("eps", ctypes.c_float),
+        ("out_adv", _P), ("out_ratio", _P), ("out_term", _P), ("out_rollout_obj", _P),
+        ("out_group_obj", _P), ("out_skipped", _P), ("out_J", _P),
+        ("stream", _P),
+    ]
+
+
 class ForkError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__("fork_step failed (%d): %s" % (code, msg))
@@ -86,6 +107,14 @@ def lib():
         L.fork_release.argtypes = []
         L.fork_version.restype = ctypes.c_int
         L.fork_version.argtypes = []
+        L.fork_logprob.restype = ctypes.c_int
+        L.fork_logprob.argtypes = [ctypes.POINTER(ForkLogprobArgs)]
+        L.fork_logprob_workspace_bytes.restype = ctypes.c_size_t
+        L.fork_logprob_workspace_bytes.argtypes = [_I32, _I32]
+        L.fork_grpo_objective.restype = ctypes.c_int
+        L.fork_grpo_objective.argtypes = [ctypes.POINTER(ForkGrpoArgs)]
+        L.fork_top_entropy.restype = ctypes.c_int
+        L.fork_top_entropy.argtypes = [_P, _I32, _I32, _I32, _P, _P]
         _lib = L
     return _lib
 
@@ -187,6 +216,98 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
     rc = lib().fork_step_ex(ctypes.byref(a))
     if rc != FORK_OK:
         raise ForkError(rc, lib().fork_last_error().decode())
+
+
+def _raise_on(rc: int) -> None:
+    if rc != FORK_OK:
+        raise ForkError(rc, lib().fork_last_error().decode())
+
+
+def logprob(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tensor,
+            out_logp: torch.Tensor, *, rows: Optional[torch.Tensor] = None, out_q=None,
+            out_entropy=None, out_lse=None, workspace=None, stream=None, events=None) -> None:
+    """fork_logprob of the C ABI: log q(tokens[e]) at hidden row rows[e]
+    (row e without ``rows``) under W_head."""
+    if hidden.dim() != 2 or W_head.dim() != 2:
+        raise ValueError("hidden and W_head must be 2-D")
+    device = hidden.device
+    if device.type != "cuda":
+        raise ValueError("fork_logprob runs on the GPU; hidden is on %s" % device)
+    M, d = hidden.shape
+    V = W_head.shape[0]
+    n = tokens.numel()
+    if hidden.dtype == torch.bfloat16:
+        dt = FORK_BF16
+    elif hidden.dtype == torch.float32:
+        dt = FORK_F32
+    else:
+        raise TypeError("hidden must be bfloat16 or float32")
+    a = ForkLogprobArgs()
+    a.hidden = _check(hidden, "hidden", hidden.dtype, M * d, device)
+    a.W_head = _check(W_head, "W_head", hidden.dtype, V * d, device)
+    a.rows = _opt(rows, "rows", torch.int32, n, device)
+    a.tokens = _check(tokens, "tokens", torch.int32, n, device)
+    a.out_logp = _check(out_logp, "out_logp", torch.float32, n, device)
+    a.out_q = _opt(out_q, "out_q", torch.float32, n, device)
+    a.out_entropy = _opt(out_entropy, "out_entropy", torch.float32, n, device)
+    a.out_lse = _opt(out_lse, "out_lse", torch.float32, n, device)
+    a.n, a.M, a.d, a.V, a.dtype = n, M, d, V, dt
+    a.stream = _stream_handle(stream, device)
+    if workspace is not None:
+        a.workspace = workspace.data_ptr()
+        a.workspace_bytes = workspace.numel() * workspace.element_size()
+    if events is not None:
+        a.ev_lmhead_begin, a.ev_lmhead_end = events
+    _raise_on(lib().fork_logprob(ctypes.byref(a)))
+
+
+def grpo_objective(rewards: torch.Tensor, offsets: torch.Tensor, lp_new: torch.Tensor,
+                   lp_old: torch.Tensor, G: int, eps: float, out_group_obj: torch.Tensor,
+                   out_skipped: torch.Tensor, out_J: torch.Tensor, *, out_adv=None,
+                   out_ratio=None, out_term=None, out_rollout_obj=None, stream=None) -> None:
+    """fork_grpo_objective of the C ABI (rewards [n_groups*G], offsets
+    [n_groups*G + 1], lp_new / lp_old [n])."""
+    device = rewards.device
+    if device.type != "cuda":
+        raise ValueError("fork_grpo_objective runs on the GPU")
+    R = rewards.numel()
+    if R % G:
+        raise ValueError("rewards must hold n_groups * G entries")
+    ng = R // G
+    n = lp_new.numel()
+    a = ForkGrpoArgs()
+    a.n_groups, a.G, a.n = ng, int(G), n
+    a.rewards = _check(rewards, "rewards", torch.float32, R, device)
+    a.offsets = _check(offsets, "offsets", torch.int32, R + 1, device)
+    a.lp_new = _check(lp_new, "lp_new", torch.float32, n, device)
+    a.lp_old = _check(lp_old, "lp_old", torch.float32, n, device)
+    a.eps = float(eps)
+    a.out_adv = _opt(out_adv, "out_adv", torch.float32, R, device)
+    a.out_ratio = _opt(out_ratio, "out_ratio", torch.float32, n, device)
+    a.out_term = _opt(out_term, "out_term", torch.float32, n, device)
+    a.out_rollout_obj = _opt(out_rollout_obj, "out_rollout_obj", torch.float32, R, device)
+    a.out_group_obj = _check(out_group_obj, "out_group_obj", torch.float32, ng, device)
+    a.out_skipped = _check(out_skipped, "out_skipped", torch.uint8, ng, device)
+    a.out_J = _check(out_J, "out_J", torch.float32, 1, device)
+    a.stream = _stream_handle(stream, device)
+    _raise_on(lib().fork_grpo_objective(ctypes.byref(a)))
+
+
+def top_entropy(entropy: torch.Tensor, k: int, out_sel: torch.Tensor, stream=None) -> None:
+    """fork_top_entropy of the C ABI on an [R, Lg] float32 tensor."""
+    if entropy.dim() != 2:
+        raise ValueError("entropy must be [R, Lg]")
+    device = entropy.device
+    if device.type != "cuda":
+        raise ValueError("fork_top_entropy runs on the GPU")
+    R, Lg = entropy.shape
+    e = _check(entropy, "entropy", torch.float32, R * Lg, device)
+    o = _check(out_sel, "out_sel", torch.uint8, R * Lg, device)
+    _raise_on(lib().fork_top_entropy(e, R, Lg, int(k), o, _stream_handle(stream, device)))
+
+
+def logprob_workspace_bytes(n: int, V: int) -> int:
+    return int(lib().fork_logprob_workspace_bytes(n, V))
 
 
 def workspace_bytes(B: int, L: int, V: int) -> int:

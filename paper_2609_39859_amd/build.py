@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libforkstep.so")
-SOURCES = ["gemm_stats.hip", "merge_select.hip", "fork_abi.hip"]
+SOURCES = ["gemm_stats.hip", "merge_select.hip", "grpo.hip", "fork_abi.hip"]
 ARCH = "gfx950"
 
 

@@ -181,14 +181,14 @@ int fork_step_ex(const fork_step_args* a) {
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_gemm_stats(a->hidden, a->W_head, a->dtype == FORK_BF16, M, a->d, a->V,
-                              partials, rowlist, Mh, sa, stream);
+                              partials, rowlist, Mh, sa, fork::TargetArgs{}, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "gemm_stats launch: %s", hipGetErrorString(e));
   if (a->ev_lmhead_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_end), stream);
     if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = fork::launch_merge(partials, M, nvt, a->out_conf, a->out_entropy, a->out_logp, a->out_lse,
-                         argmax, rowlist, sa.row, sa.partials, stream);
+                         argmax, rowlist, sa.row, sa.partials, nullptr, nullptr, a->V, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
   e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf,
                           a->out_entropy, a->fallback_uniform, argmax, a->tokens, a->mask,
@@ -231,6 +231,111 @@ int fork_step(const void* hidden, const void* W_head, int32_t* tokens, uint8_t* 
   a.stream = stream;
   a.rule = FORK_RULE_LEFTMOST;
   return fork_step_ex(&a);
+}
+
+// fork_logprob workspace: [partials: nvt*n float4][target logits: n float].
+static bool logprob_layout(int32_t n, int32_t V, size_t* zt_off, size_t* total) {
+  if (n < 0 || V <= 0) return false;
+  const size_t nvt = (size_t)fork::num_vocab_tiles(V);
+  *zt_off = align_up(nvt * (size_t)n * sizeof(float4));
+  *total = *zt_off + align_up((size_t)n * sizeof(float));
+  return true;
+}
+
+size_t fork_logprob_workspace_bytes(int32_t n, int32_t V) {
+  size_t zt, total;
+  return logprob_layout(n, V, &zt, &total) ? total : 0;
+}
+
+int fork_logprob(const fork_logprob_args* a) {
+  if (!a) return fail(FORK_EINVAL, "args is NULL");
+  if (a->n < 0 || a->M <= 0 || a->d <= 0 || a->V <= 0)
+    return fail(FORK_EINVAL, "sizes must be positive (n=%d M=%d d=%d V=%d)", a->n, a->M, a->d,
+                a->V);
+  if (a->dtype != FORK_BF16 && a->dtype != FORK_F32)
+    return fail(FORK_EINVAL, "unknown dtype %d", a->dtype);
+  if (!a->hidden || !a->W_head || (a->n > 0 && (!a->tokens || !a->out_logp)))
+    return fail(FORK_EINVAL, "a required pointer is NULL");
+  if (!a->rows && a->n > a->M)
+    return fail(FORK_EINVAL, "without rows, n=%d entries need n <= M=%d", a->n, a->M);
+  if (a->dtype == FORK_BF16 && a->d % 8 != 0)
+    return fail(FORK_EUNSUPPORTED, "bf16 path needs d %% 8 == 0 (d=%d)", a->d);
+  if (a->dtype == FORK_F32 && a->d % 4 != 0)
+    return fail(FORK_EUNSUPPORTED, "fp32 path needs d %% 4 == 0 (d=%d)", a->d);
+  if (a->d > kMaxD)
+    return fail(FORK_EUNSUPPORTED, "d=%d exceeds the supported maximum %d", a->d, kMaxD);
+  if (a->rows && (long long)a->M * a->d * (a->dtype == FORK_BF16 ? 2 : 4) >= (1LL << 31))
+    return fail(FORK_EUNSUPPORTED, "gathered rows need M*d*element_size < 2^31");
+  if (!aligned16(a->hidden) || !aligned16(a->W_head))
+    return fail(FORK_EINVAL, "hidden and W_head must be 16-byte aligned");
+  size_t zt_off, total;
+  if (!logprob_layout(a->n, a->V, &zt_off, &total)) return fail(FORK_EINVAL, "invalid sizes");
+  if (a->n == 0) return FORK_OK;
+  void* ws = a->workspace;
+  if (ws) {
+    if (a->workspace_bytes < total)
+      return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, total);
+    if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
+  } else {
+    int rc = get_workspace(total, &ws);
+    if (rc != FORK_OK) return rc;
+  }
+  float4* partials = static_cast<float4*>(ws);
+  float* ztoken = reinterpret_cast<float*>(static_cast<char*>(ws) + zt_off);
+  hipStream_t stream = static_cast<hipStream_t>(a->stream);
+  const int nvt = fork::num_vocab_tiles(a->V);
+  hipError_t e;
+  if (a->ev_lmhead_begin) {
+    e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_begin), stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  e = fork::launch_gemm_stats(a->hidden, a->W_head, a->dtype == FORK_BF16, a->n, a->d, a->V,
+                              partials, a->rows, a->M, fork::SampleArgs{},
+                              fork::TargetArgs{a->tokens, ztoken}, stream);
+  if (e != hipSuccess) return fail(FORK_EHIP, "gemm_stats launch: %s", hipGetErrorString(e));
+  if (a->ev_lmhead_end) {
+    e = hipEventRecord(static_cast<hipEvent_t>(a->ev_lmhead_end), stream);
+    if (e != hipSuccess) return fail(FORK_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  e = fork::launch_merge(partials, a->n, nvt, a->out_q, a->out_entropy, a->out_logp, a->out_lse,
+                         nullptr, nullptr, nullptr, nullptr, a->tokens, ztoken, a->V, stream);
+  if (e != hipSuccess) return fail(FORK_EHIP, "merge launch: %s", hipGetErrorString(e));
+  return FORK_OK;
+}
+
+int fork_grpo_objective(const fork_grpo_args* a) {
+  if (!a) return fail(FORK_EINVAL, "args is NULL");
+  if (a->n_groups < 0 || a->G <= 0 || a->n < 0)
+    return fail(FORK_EINVAL, "sizes must be non-negative, G positive (n_groups=%d G=%d n=%d)",
+                a->n_groups, a->G, a->n);
+  if (a->G > fork::kMaxGroupSize)
+    return fail(FORK_EINVAL, "G=%d exceeds the supported maximum %d", a->G, fork::kMaxGroupSize);
+  if ((long long)a->n_groups * a->G > 0x7ffffffeLL) return fail(FORK_EINVAL, "too many rollouts");
+  if (!(a->eps >= 0.0f) || !isfinite(a->eps))
+    return fail(FORK_EINVAL, "eps must be finite and >= 0");
+  if (!a->out_J || (a->n_groups > 0 && (!a->rewards || !a->offsets || !a->out_group_obj ||
+                                         !a->out_skipped)) ||
+      (a->n > 0 && (!a->lp_new || !a->lp_old)))
+    return fail(FORK_EINVAL, "a required pointer is NULL");
+  hipError_t e = fork::launch_grpo_objective(
+      a->n_groups, a->G, a->n, a->rewards, a->offsets, a->lp_new, a->lp_old, a->eps, a->out_adv,
+      a->out_ratio, a->out_term, a->out_rollout_obj, a->out_group_obj, a->out_skipped, a->out_J,
+      static_cast<hipStream_t>(a->stream));
+  if (e != hipSuccess) return fail(FORK_EHIP, "grpo launch: %s", hipGetErrorString(e));
+  return FORK_OK;
+}
+
+int fork_top_entropy(const float* entropy, int32_t R, int32_t Lg, int32_t k, uint8_t* sel,
+                     void* stream) {
+  if (R < 0 || Lg <= 0 || k < 0 || k > Lg)
+    return fail(FORK_EINVAL, "need R >= 0, Lg > 0, 0 <= k <= Lg (R=%d Lg=%d k=%d)", R, Lg, k);
+  if (Lg > fork::kMaxTopEntropyLen)
+    return fail(FORK_EUNSUPPORTED, "Lg=%d exceeds the supported maximum %d", Lg,
+                fork::kMaxTopEntropyLen);
+  if (R > 0 && (!entropy || !sel)) return fail(FORK_EINVAL, "a required pointer is NULL");
+  hipError_t e = fork::launch_top_entropy(R, Lg, k, entropy, sel, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FORK_EHIP, "top_entropy launch: %s", hipGetErrorString(e));
+  return FORK_OK;
 }
 
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V) {

@@ -33,26 +33,40 @@ struct SampleArgs {
   uint32_t key0, key1, counter;
 };
 
+// Teacher-forced mode: token[p] is a vocabulary index per LM-head position;
+// the epilogue stores that entry's logit to z[p] (tokens outside [0, V)
+// store nothing).
+struct TargetArgs {
+  const int32_t* token;
+  float* z;
+};
+
 inline int num_vocab_tiles(int V) { return (V + kTileV - 1) / kTileV; }
 inline int num_pos_tiles(int M) { return (M + kTileP - 1) / kTileP; }
 
 // Logits of M positions against W (never stored) reduced to one Partial per
 // (vocabulary tile, position): partials[vt * M + p].  Position p is hidden row
 // p, or with a row list hidden row rowlist[p] (-1 = none) out of Mh rows.
+// At most one of sample.row and target.token may be set.
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16,
                              int M, int d, int V, float4* partials,
                              const int32_t* rowlist, int Mh, const SampleArgs& sample,
-                             hipStream_t stream);
+                             const TargetArgs& target, hipStream_t stream);
 
 // Merge the partials of each position over all vocabulary tiles into the
 // per-position results (position p lands in row p, or rowlist[p] if a row
 // list is given; -1 = dropped).  lse may be null.  Positions with
 // sample_row[p] >= 0 (sample_row may be null) take the drawn candidate from
 // spartials, with the untempered confidence and log-probability of it.
+//
+// Teacher-forced mode (token non-null): logp and conf are log q and q of
+// token[p] from its logit ztoken[p] (NaN for a token outside [0, V)).  Any of
+// conf, entropy, lse, argmax may be null.
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse,
                         int32_t* argmax, const int32_t* rowlist,
                         const int32_t* sample_row, const float4* spartials,
+                        const int32_t* token, const float* ztoken, int V,
                         hipStream_t stream);
 
 // Rows of each sequence's active block (the same skip-forward as the
@@ -71,5 +85,22 @@ hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          int32_t* tokens, uint8_t* mask, int32_t* block_start,
                          int32_t* fallback, int32_t* ncommit,
                          int32_t* commit_pos, hipStream_t stream);
+
+// ForkGRPO objective over n_groups groups of G rollouts (G <=
+// kMaxGroupSize); entries of rollout i are [offsets[i], offsets[i+1])
+// clamped to [0, n).  adv, ratio, term, rollout_obj may be null; group_obj,
+// skipped ([n_groups]) and J ([1]) are written.
+constexpr int kMaxGroupSize = 1024;
+hipError_t launch_grpo_objective(int n_groups, int G, int n, const float* rewards,
+                                 const int32_t* offsets, const float* lp_new,
+                                 const float* lp_old, float eps, float* adv, float* ratio,
+                                 float* term, float* rollout_obj, float* group_obj,
+                                 uint8_t* skipped, float* J, hipStream_t stream);
+
+// Per rollout (R of them, Lg <= kMaxTopEntropyLen positions each) the k
+// positions of highest entropy, ties in increasing position: sel = 1 there.
+constexpr int kMaxTopEntropyLen = 16384;
+hipError_t launch_top_entropy(int R, int Lg, int k, const float* entropy, uint8_t* sel,
+                              hipStream_t stream);
 
 }  // namespace fork

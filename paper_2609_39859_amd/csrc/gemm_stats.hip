@@ -146,13 +146,18 @@ __device__ __forceinline__ int acc_row(int i, int e, int lane) {
 
 // Per-(position, tile) statistics from the accumulators of one wave, combined
 // across the two vocabulary waves through LDS, stored to partials.
-// Drawn candidates (kDraw) go through a second LDS exchange and a second
-// partials array (see SampleArgs).
-template <bool kDraw>
+// What the epilogue produces besides the per-tile statistics.
+enum EpilogueMode { kGreedy = 0, kDrawn = 1, kTarget = 2 };
+
+// Drawn candidates (kDrawn) go through a second LDS exchange and a second
+// partials array (see SampleArgs); the logit of a given token (kTarget) is
+// stored by the one lane that holds it.
+template <int kMode>
 __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned char* smem, int tid,
                                          int lane, int wv, int wp, int vt, int v0, int p0, int M,
                                          int V, float4* __restrict__ partials,
-                                         const SampleArgs& sa) {
+                                         const SampleArgs& sa, const TargetArgs& ta) {
+  constexpr bool kDraw = kMode == kDrawn;
   float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
   float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
   const int vbase = v0 + wv * 128;
@@ -200,6 +205,22 @@ __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned cha
     t += __shfl_xor(t, 32);
     const int col = wp * 64 + j * 32 + (lane & 31);
     if (lane < 32) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
+    if (kMode == kTarget) {
+      const int tk = p0 + col < M ? ta.token[p0 + col] : -1;
+      if (tk >= vbase && tk < vbase + 128 && tk < V) {
+        float zt = 0.f;
+        bool hit = false;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (vbase + acc_row(i, e, lane) == tk) {
+              zt = acc[i][j][e];
+              hit = true;
+            }
+        if (hit) ta.z[p0 + col] = zt;
+      }
+    }
     if (kDraw) {
       const int srow = p0 + col < M ? sa.row[p0 + col] : -1;
       if (__ballot(srow >= 0)) {
@@ -271,11 +292,11 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-template <bool kDraw>
+template <int kMode>
 __device__ __forceinline__ void gemm_stats_bf16_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
     int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
-    int Mh, const SampleArgs& sa) {
+    int Mh, const SampleArgs& sa, const TargetArgs& ta) {
   // W ring: slots 0..2; hidden ring: slots 3..4
   __shared__ __attribute__((aligned(1024))) unsigned char smem[5 * kOperandBytes];
 
@@ -298,7 +319,8 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   // W / hidden are outside the record count and read as zero.
   const unsigned recW = (unsigned)(min(kTileV, V - v0) * row_bytes);
   // With a row list, position p of the tile is hidden row rowlist[p0 + p]
-  // (-1: no row, reads as zero) and the descriptor spans all Mh rows.
+  // (outside [0, Mh): no row, reads as zero) and the descriptor spans all Mh
+  // rows.
   const unsigned recH = rowlist ? (unsigned)(Mh * row_bytes)
                                 : (unsigned)(min(kTileP, M - p0) * row_bytes);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
@@ -326,8 +348,9 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     if (rowlist) {
       const int p = p0 + drow + 8 * q;
       const int r = p < M ? rowlist[p] : -1;
-      hoff[q] = r >= 0 ? (unsigned)(r * row_bytes) + (unsigned)(((q & 1) ? dchunk1 : dchunk0) << 4)
-                       : kOutOfRange;
+      hoff[q] = (r >= 0 && r < Mh)
+                    ? (unsigned)(r * row_bytes) + (unsigned)(((q & 1) ? dchunk1 : dchunk0) << 4)
+                    : kOutOfRange;
     }
   }
   const int kfull = kchunks >> 3;  // stages whose chunks all lie inside d
@@ -470,16 +493,16 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
-  epilogue<kDraw>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa);
+  epilogue<kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
 }
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
 // 16-byte chunk.
-template <bool kDraw>
+template <int kMode>
 __device__ __forceinline__ void gemm_stats_f32_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
     int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
-    int Mh, const SampleArgs& sa) {
+    int Mh, const SampleArgs& sa, const TargetArgs& ta) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * kOperandBytes];
 
   const int tid = threadIdx.x;
@@ -507,7 +530,9 @@ __device__ __forceinline__ void gemm_stats_f32_body(
     // Rows past the end re-read the last row; their results are discarded.
     const int vr = min(v0 + r0 + 64 * i, V - 1);
     int pr = min(p0 + r0 + 64 * i, M - 1);
-    if (rowlist) pr = max(rowlist[pr], 0);  // positions without a row: any valid row
+    // positions without a valid row read row 0 (their results are dropped
+    // or unspecified); rows stay inside hidden
+    if (rowlist) pr = min(max(rowlist[pr], 0), Mh - 1);
     ga[i] = W + (size_t)vr * row_bytes + (c << 4);
     gb[i] = hidden + (size_t)pr * row_bytes + (c << 4);
   }
@@ -573,56 +598,75 @@ __device__ __forceinline__ void gemm_stats_f32_body(
     __syncthreads();
   }
 
-  epilogue<kDraw>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa);
+  epilogue<kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
 }
 
 // Entry points: positions = hidden rows 0..M-1, or gathered through a row
-// list (the active-block rows); greedy candidates only, or drawn candidates
-// as well.  Separate symbols keep the row-list and drawing code out of the
-// dense greedy kernel and the variants apart in kernel traces.
+// list; greedy candidates only, drawn candidates as well, or the logits of
+// given tokens.  Separate symbols keep the row-list, drawing and target code
+// out of the dense greedy kernel and the variants apart in kernel traces.
+#define FORK_GEMM_ARGS                                                                         \
+  const unsigned char *__restrict__ hidden, const unsigned char *__restrict__ W, int M, int d, \
+      int V, int nvt, int npt, float4 *__restrict__ partials
 #define FORK_GEMM_ENTRIES(T)                                                                   \
-  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_kernel(                        \
-      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
-      int d, int V, int nvt, int npt, float4* __restrict__ partials) {                         \
-    gemm_stats_##T##_body<false>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M,           \
-                                 SampleArgs{});                                                \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_kernel(FORK_GEMM_ARGS) {       \
+    gemm_stats_##T##_body<kGreedy>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M,         \
+                                   SampleArgs{}, TargetArgs{});                                \
   }                                                                                            \
   __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_kernel(                   \
-      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
-      int d, int V, int nvt, int npt, float4* __restrict__ partials,                           \
-      const int32_t* __restrict__ rowlist, int Mh) {                                           \
-    gemm_stats_##T##_body<false>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh,          \
-                                 SampleArgs{});                                                \
+      FORK_GEMM_ARGS, const int32_t* __restrict__ rowlist, int Mh) {                           \
+    gemm_stats_##T##_body<kGreedy>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh,        \
+                                   SampleArgs{}, TargetArgs{});                                \
   }                                                                                            \
-  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_draw_kernel(                   \
-      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
-      int d, int V, int nvt, int npt, float4* __restrict__ partials, SampleArgs sa) {          \
-    gemm_stats_##T##_body<true>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M, sa);       \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_draw_kernel(FORK_GEMM_ARGS,    \
+                                                                          SampleArgs sa) {     \
+    gemm_stats_##T##_body<kDrawn>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M, sa,      \
+                                  TargetArgs{});                                               \
   }                                                                                            \
   __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_draw_kernel(              \
-      const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M,    \
-      int d, int V, int nvt, int npt, float4* __restrict__ partials,                           \
-      const int32_t* __restrict__ rowlist, int Mh, SampleArgs sa) {                            \
-    gemm_stats_##T##_body<true>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh, sa);      \
+      FORK_GEMM_ARGS, const int32_t* __restrict__ rowlist, int Mh, SampleArgs sa) {            \
+    gemm_stats_##T##_body<kDrawn>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh, sa,     \
+                                  TargetArgs{});                                               \
+  }                                                                                            \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_target_kernel(FORK_GEMM_ARGS,  \
+                                                                            TargetArgs ta) {   \
+    gemm_stats_##T##_body<kTarget>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M,         \
+                                   SampleArgs{}, ta);                                          \
+  }                                                                                            \
+  __global__ __launch_bounds__(kThreads) void gemm_stats_##T##_rows_target_kernel(            \
+      FORK_GEMM_ARGS, const int32_t* __restrict__ rowlist, int Mh, TargetArgs ta) {            \
+    gemm_stats_##T##_body<kTarget>(hidden, W, M, d, V, nvt, npt, partials, rowlist, Mh,        \
+                                   SampleArgs{}, ta);                                          \
   }
 FORK_GEMM_ENTRIES(bf16)
 FORK_GEMM_ENTRIES(f32)
+#undef FORK_GEMM_ARGS
 #undef FORK_GEMM_ENTRIES
 
 }  // namespace
 
 hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M, int d, int V,
                              float4* partials, const int32_t* rowlist, int Mh,
-                             const SampleArgs& sample, hipStream_t stream) {
+                             const SampleArgs& sample, const TargetArgs& target,
+                             hipStream_t stream) {
   const int nvt = num_vocab_tiles(V);
   const int npt = num_pos_tiles(M);
   const dim3 grid((unsigned)(nvt * npt)), block(kThreads);
   const auto* h = static_cast<const unsigned char*>(hidden);
   const auto* w = static_cast<const unsigned char*>(W);
   const bool draw = sample.row != nullptr;
+  const bool tgt = target.token != nullptr;
 #define FORK_LAUNCH(K, ...) hipLaunchKernelGGL(K, grid, block, 0, stream, h, w, M, d, V, nvt, npt, \
                                                partials, ##__VA_ARGS__)
-  if (bf16 && rowlist && draw)
+  if (bf16 && rowlist && tgt)
+    FORK_LAUNCH(gemm_stats_bf16_rows_target_kernel, rowlist, Mh, target);
+  else if (bf16 && tgt)
+    FORK_LAUNCH(gemm_stats_bf16_target_kernel, target);
+  else if (!bf16 && rowlist && tgt)
+    FORK_LAUNCH(gemm_stats_f32_rows_target_kernel, rowlist, Mh, target);
+  else if (!bf16 && tgt)
+    FORK_LAUNCH(gemm_stats_f32_target_kernel, target);
+  else if (bf16 && rowlist && draw)
     FORK_LAUNCH(gemm_stats_bf16_rows_draw_kernel, rowlist, Mh, sample);
   else if (bf16 && rowlist)
     FORK_LAUNCH(gemm_stats_bf16_rows_kernel, rowlist, Mh);

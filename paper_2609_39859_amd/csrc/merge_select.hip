@@ -58,7 +58,8 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
     const float4* __restrict__ partials, int M, int nvt, float* __restrict__ conf,
     float* __restrict__ entropy, float* __restrict__ logp, float* __restrict__ lse,
     int32_t* __restrict__ argmax, const int32_t* __restrict__ rowlist,
-    const int32_t* __restrict__ sample_row, const float4* __restrict__ spartials) {
+    const int32_t* __restrict__ sample_row, const float4* __restrict__ spartials,
+    const int32_t* __restrict__ token, const float* __restrict__ ztoken, int V) {
   __shared__ float4 red[kMergeWaves][kMergeRows];
   __shared__ float4 sred[kMergeWaves][kMergeRows];
   const int lane = threadIdx.x & 63;
@@ -82,9 +83,16 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
 #pragma unroll
     for (int k = 1; k < kMergeWaves; ++k) acc = merge2(acc, red[k][lane]);
     const float log_s = logf(acc.y);
-    entropy[dst] = log_s - acc.z / acc.y;
+    if (entropy) entropy[dst] = log_s - acc.z / acc.y;
     if (lse) lse[dst] = acc.x + log_s;
-    if (drawn) {
+    if (argmax) argmax[dst] = __float_as_int(acc.w);
+    if (token) {
+      // teacher-forced: log q of the given token from its logit
+      const int tk = token[r];
+      const float lq = (tk >= 0 && tk < V) ? (ztoken[r] - acc.x) - log_s : __int_as_float(0x7fc00000);
+      logp[dst] = lq;
+      if (conf) conf[dst] = exp2f(lq * kLog2e);
+    } else if (drawn) {
 #pragma unroll
       for (int k = 1; k < kMergeWaves; ++k) sacc = pick_drawn(sacc, sred[k][lane]);
       // untempered q of the drawn token: exp(z - m) / s
@@ -93,9 +101,8 @@ __global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
       logp[dst] = dz - log_s;
       argmax[dst] = __float_as_int(sacc.y);
     } else {
-      conf[dst] = 1.0f / acc.y;
+      if (conf) conf[dst] = 1.0f / acc.y;
       logp[dst] = -log_s;
-      argmax[dst] = __float_as_int(acc.w);
     }
   }
 }
@@ -292,11 +299,13 @@ hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
 hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         float* entropy, float* logp, float* lse, int32_t* argmax,
                         const int32_t* rowlist, const int32_t* sample_row,
-                        const float4* spartials, hipStream_t stream) {
+                        const float4* spartials, const int32_t* token, const float* ztoken,
+                        int V, hipStream_t stream) {
   const dim3 grid((unsigned)((M + kMergeRows - 1) / kMergeRows));
   const dim3 block(kMergeRows * kMergeWaves);
   hipLaunchKernelGGL(merge_kernel, grid, block, 0, stream, partials, M, nvt, conf,
-                     entropy, logp, lse, argmax, rowlist, sample_row, spartials);
+                     entropy, logp, lse, argmax, rowlist, sample_row, spartials, token, ztoken,
+                     V);
   return hipGetLastError();
 }
 

@@ -88,6 +88,15 @@ CONFIGS["tiny_peaked"] = CONFIGS["tiny"].with_(name="tiny_peaked",
                                                scale_args=(0.05, 3.0))
 CONFIGS["mid_planted"] = CONFIGS["mid"].with_(name="mid_planted", tau=0.5,
                                               plant_peaks=0.5)
+# ForkGRPO rollouts in the paper's shape of a batch (groups of G = 16
+# rollouts per prompt, lambda = 0.8, blocks of 32), scaled down so that the
+# oracle follows a whole decode: 2 prompts x 16 rollouts, 64 generated
+# positions, d = 128, V = 1024; planted peaks give a mix of parallel and
+# fallback steps.
+CONFIGS["grpo_small"] = SynthConfig("grpo_small", B=32, P=16, G=64, block_len=32, d=128,
+                                    V=1024, dtype="bf16", tau=0.8,
+                                    scale_kind="temp_loguniform", scale_args=(0.1, 4.0),
+                                    plant_peaks=0.15)
 
 
 def _gen(seed: int, device) -> torch.Generator:

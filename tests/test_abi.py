@@ -112,3 +112,88 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(4, 8, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         _binding.fork_step(x, x, None, None, None, 1, 0.5, None, None, None, None, B=1, L=4)
+
+
+def test_grpo_entry_points_declared():
+    names = _declared_functions()
+    for n in ("fork_logprob", "fork_logprob_workspace_bytes", "fork_grpo_objective",
+              "fork_top_entropy"):
+        assert n in names
+
+
+def test_logprob_workspace_sizes():
+    L = _binding.lib()
+    pad = lambda x: (x + 255) // 256 * 256
+    for n, V in [(1, 1), (4096, 126464), (37, 1013)]:
+        nvt = (V + 255) // 256
+        assert L.fork_logprob_workspace_bytes(n, V) == pad(nvt * n * 16) + pad(n * 4)
+    assert L.fork_logprob_workspace_bytes(-1, 5) == 0
+    assert L.fork_logprob_workspace_bytes(5, 0) == 0
+
+
+def _lp_args(**kw):
+    a = _binding.ForkLogprobArgs()
+    good = dict(hidden=16, W_head=32, rows=48, tokens=64, out_logp=80, n=4, M=8, d=16, V=100,
+                dtype=_binding.FORK_BF16)
+    good.update(kw)
+    for k, v in good.items():
+        assert hasattr(a, k)
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hidden=0), _binding.FORK_EINVAL),
+    (dict(tokens=0), _binding.FORK_EINVAL),
+    (dict(out_logp=0), _binding.FORK_EINVAL),
+    (dict(n=-1), _binding.FORK_EINVAL),
+    (dict(M=0), _binding.FORK_EINVAL),
+    (dict(V=0), _binding.FORK_EINVAL),
+    (dict(dtype=3), _binding.FORK_EINVAL),
+    (dict(rows=0, n=9), _binding.FORK_EINVAL),        # n > M without a row list
+    (dict(d=12), _binding.FORK_EUNSUPPORTED),
+    (dict(M=1 << 20, d=2048), _binding.FORK_EUNSUPPORTED),  # gathered rows past 2^31 bytes
+    (dict(hidden=18), _binding.FORK_EINVAL),
+    (dict(workspace=256, workspace_bytes=10), _binding.FORK_EINVAL),
+])
+def test_logprob_bad_arguments_rejected_on_host(kw, code):
+    L = _binding.lib()
+    assert L.fork_logprob(ctypes.byref(_lp_args(**kw))) == code
+    assert L.fork_last_error().decode() != ""
+
+
+def test_logprob_zero_entries_is_a_no_op():
+    L = _binding.lib()
+    assert L.fork_logprob(ctypes.byref(_lp_args(n=0, tokens=0, out_logp=0))) == _binding.FORK_OK
+
+
+def _grpo_args(**kw):
+    a = _binding.ForkGrpoArgs()
+    good = dict(n_groups=2, G=4, n=10, rewards=16, offsets=32, lp_new=48, lp_old=64, eps=0.2,
+                out_group_obj=80, out_skipped=96, out_J=112)
+    good.update(kw)
+    for k, v in good.items():
+        assert hasattr(a, k)
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("kw", [
+    dict(G=0), dict(n_groups=-1), dict(n=-2), dict(G=1025), dict(eps=-0.1),
+    dict(eps=float("nan")), dict(eps=float("inf")), dict(out_J=0), dict(rewards=0),
+    dict(offsets=0), dict(out_group_obj=0), dict(out_skipped=0), dict(lp_new=0),
+])
+def test_grpo_bad_arguments_rejected_on_host(kw):
+    L = _binding.lib()
+    assert L.fork_grpo_objective(ctypes.byref(_grpo_args(**kw))) == _binding.FORK_EINVAL
+    assert L.fork_last_error().decode() != ""
+
+
+@pytest.mark.parametrize("R,Lg,k,ptr,code", [
+    (2, 0, 0, 16, _binding.FORK_EINVAL), (-1, 8, 1, 16, _binding.FORK_EINVAL),
+    (2, 8, 9, 16, _binding.FORK_EINVAL), (2, 8, -1, 16, _binding.FORK_EINVAL),
+    (2, 8, 1, 0, _binding.FORK_EINVAL), (2, 16385, 1, 16, _binding.FORK_EUNSUPPORTED),
+])
+def test_top_entropy_bad_arguments_rejected_on_host(R, Lg, k, ptr, code):
+    L = _binding.lib()
+    assert L.fork_top_entropy(ptr, R, Lg, k, ptr, None) == code

@@ -1,0 +1,288 @@
+"""GPU parity of the ForkGRPO side (Section 3.2): teacher-forced
+log-probabilities through the target LM-head kernels, the clipped surrogate
+objective, JustGRPO-Fast's top-entropy selection, and a whole rollout batch
+in lock-step with the oracle followed by the objective under a perturbed
+head.  Every call goes through the C ABI; expected values come from the
+oracle only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39859_amd import _binding, synth
+
+from harness import STAT_TOL, compare_sampled, gpu_step, host_bits
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+OBJ_TOL = 1e-5          # fp32 objective against binary64, same inputs
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _logprob(h, W, rows, toks):
+    n = toks.numel()
+    f = lambda: torch.full((n,), float("nan"), device=DEV)
+    lp, q, ent, lse = f(), f(), f(), f()
+    _binding.logprob(h, W, toks, lp, rows=rows, out_q=q, out_entropy=ent, out_lse=lse)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in (("logp", lp), ("q", q), ("entropy", ent), ("lse", lse))}
+
+
+SHAPES = [
+    # M, d, V, dtype, n, with_rows
+    (37, 200, 1013, torch.bfloat16, 50, True),
+    (300, 72, 257, torch.float32, 300, False),
+    (61, 520, 2049, torch.bfloat16, 61, False),
+    (129, 1032, 777, torch.bfloat16, 400, True),
+    (5, 8, 1, torch.bfloat16, 3, True),
+    (257, 96, 300, torch.float32, 90, True),
+]
+
+
+@pytest.mark.parametrize("M,d,V,dtype,n,with_rows", SHAPES)
+def test_logprob_matches_oracle(M, d, V, dtype, n, with_rows):
+    """Random rows (repeats included) and tokens (0 and V-1 included) on
+    ragged shapes; log q, q, entropy and log-normaliser against the oracle."""
+    _need_gpu()
+    gen = torch.Generator().manual_seed(M + d + V + n)
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(dtype)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(dtype)
+    rng = np.random.default_rng(M * 7 + V)
+    rows = rng.integers(0, M, n) if with_rows else np.arange(n)
+    toks = rng.integers(0, V, n)
+    toks[0], toks[-1] = 0, V - 1
+    g = _logprob(h.to(DEV), W.to(DEV),
+                 torch.as_tensor(rows, dtype=torch.int32, device=DEV) if with_rows else None,
+                 torch.as_tensor(toks, dtype=torch.int32, device=DEV))
+    ref = oracle.token_logprob(host_bits(h), host_bits(W), rows, toks)
+    st = oracle.row_stats(host_bits(h), host_bits(W), rows)
+    for k, r in (("logp", ref["logp"]), ("q", np.exp(ref["logp"])), ("entropy", ref["entropy"])):
+        err = np.abs(g[k] - r)
+        assert np.all(err <= STAT_TOL), "%s max err %g" % (k, err.max())
+    rel = np.abs(g["lse"] - st["lse"]) / np.maximum(1.0, np.abs(st["lse"]))
+    assert np.all(rel <= STAT_TOL)
+
+
+def test_logprob_invalid_token_gives_nan():
+    _need_gpu()
+    h = torch.randn(4, 16).to(torch.bfloat16).to(DEV)
+    W = torch.randn(300, 16).to(torch.bfloat16).to(DEV)
+    toks = torch.tensor([5, -1, 300, 299], dtype=torch.int32, device=DEV)
+    g = _logprob(h, W, None, toks)
+    assert np.isfinite(g["logp"][[0, 3]]).all() and np.isnan(g["logp"][[1, 2]]).all()
+
+
+def test_logprob_of_greedy_candidate_equals_step_outputs():
+    """Teacher forcing the step's own greedy candidates reproduces the
+    step's log-probability, entropy and log-normaliser bit for bit (the
+    target kernel accumulates the same products in the same order)."""
+    _need_gpu()
+    cfg = synth.CONFIGS["mid"]
+    W = synth.weights(cfg).to(DEV)
+    h = synth.hidden(cfg, 1).to(DEV)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    s = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau)
+    g = _logprob(h, W, None, torch.as_tensor(s.argmax, device=DEV))
+    for a, b in (("logp", "logp"), ("entropy", "entropy"), ("lse", "lse"), ("q", "conf")):
+        x, y = g[a], getattr(s, b)
+        if a == "q":
+            np.testing.assert_allclose(x, y, rtol=1e-5)  # exp2(-log s) vs 1/s in binary32
+        else:
+            assert np.array_equal(x.view(np.int32), y.view(np.int32)), a
+
+
+def test_logprob_full_size_sampled():
+    """4096 entries at d = 4096, V = 126464 (one ForkGRPO batch of 256
+    rollouts x 16 fallback steps): sampled entries against the oracle."""
+    _need_gpu()
+    cfg = synth.CONFIGS["llada8b"]
+    W = synth.weights(cfg, device=DEV)
+    h = synth.hidden(cfg, 4, device=DEV)
+    rng = np.random.default_rng(9)
+    toks = rng.integers(0, cfg.V, cfg.M)
+    g = _logprob(h, W, None, torch.as_tensor(toks, dtype=torch.int32, device=DEV))
+    pick = np.sort(rng.choice(cfg.M, 40, replace=False))
+    ref = oracle.token_logprob(host_bits(h), host_bits(W), pick, toks[pick])
+    assert np.all(np.abs(g["logp"][pick] - ref["logp"]) <= STAT_TOL)
+    assert np.all(np.abs(g["entropy"][pick] - ref["entropy"]) <= STAT_TOL)
+    assert np.all(np.isfinite(g["logp"])) and np.all(g["logp"] <= 1e-6)
+
+
+def _objective(rewards, offsets, lp_new, lp_old, G, eps):
+    t = lambda x, dt: torch.as_tensor(np.asarray(x), dtype=dt, device=DEV).contiguous()
+    R = len(rewards)
+    ng = R // G
+    n = len(lp_new)
+    outs = dict(out_adv=torch.empty(R, device=DEV), out_ratio=torch.empty(max(n, 0), device=DEV),
+                out_term=torch.empty(n, device=DEV), out_rollout_obj=torch.empty(R, device=DEV))
+    gobj = torch.empty(ng, device=DEV)
+    skip = torch.empty(ng, dtype=torch.uint8, device=DEV)
+    J = torch.empty(1, device=DEV)
+    _binding.grpo_objective(t(rewards, torch.float32), t(offsets, torch.int32),
+                            t(lp_new, torch.float32), t(lp_old, torch.float32), G, eps,
+                            gobj, skip, J, **outs)
+    torch.cuda.synchronize()
+    res = {k[4:]: v.cpu().numpy() for k, v in outs.items()}
+    res.update(group_obj=gobj.cpu().numpy(), skipped=skip.cpu().numpy(), J=float(J.item()))
+    return res
+
+
+def _compare_objective(g, ref):
+    for k in ("adv", "ratio", "term", "rollout_obj", "group_obj"):
+        np.testing.assert_allclose(g[k], ref[k], atol=OBJ_TOL, rtol=OBJ_TOL, err_msg=k)
+    assert np.array_equal(g["skipped"], ref["skipped"])
+    assert g["J"] == pytest.approx(ref["J"], abs=OBJ_TOL, rel=OBJ_TOL)
+
+
+def test_objective_hand_worked_fixture():
+    _need_gpu()
+    with open(os.path.join(GOLDEN, "grpo_worked.json")) as f:
+        fx = json.load(f)
+    lp_old = np.linspace(-3.0, -0.5, len(fx["ratios"])).astype(np.float32)
+    lp_new = (lp_old.astype(np.float64) + np.log(fx["ratios"])).astype(np.float32)
+    g = _objective(fx["rewards"], fx["offsets"], lp_new, lp_old, fx["G"], fx["eps"])
+    ex = fx["expected"]
+    for k in ("adv", "term", "rollout_obj", "group_obj"):
+        np.testing.assert_allclose(g[k], ex[k]["values"], atol=1e-6, err_msg=k)
+    assert g["skipped"].tolist() == ex["skipped"]
+    assert g["J"] == pytest.approx(ex["J"]["value"], abs=1e-6)
+
+
+@pytest.mark.parametrize("seed,ng,G", [(0, 16, 16), (1, 3, 5), (2, 1, 1), (3, 40, 64),
+                                       (4, 2, 1024), (5, 0, 16)])
+def test_objective_matches_oracle(seed, ng, G):
+    """Random batches (empty F_i, groups with equal rewards, large groups,
+    no groups) against the oracle on the same binary32 inputs."""
+    _need_gpu()
+    rng = np.random.default_rng(seed)
+    R = ng * G
+    nF = rng.integers(0, 25, R)
+    nF[::7] = 0
+    off = np.concatenate([[0], np.cumsum(nF)]).astype(np.int32)
+    rewards = rng.integers(0, 2, R).astype(np.float32)
+    if ng > 1:
+        rewards[:G] = 1.0
+    lp_old = (-rng.random(off[-1]) * 4).astype(np.float32)
+    lp_new = (lp_old + rng.normal(0, 0.3, off[-1])).astype(np.float32)
+    for eps in (0.2, 0.0):
+        g = _objective(rewards, off, lp_new, lp_old, G, eps)
+        ref = oracle.grpo_objective(rewards, off, lp_new, lp_old, G, eps)
+        _compare_objective(g, ref)
+
+
+@pytest.mark.parametrize("R,Lg,k", [(64, 256, 52), (64, 256, 0), (64, 256, 256), (3, 1, 1),
+                                    (5, 300, 7), (2, 16384, 3277)])
+def test_top_entropy_matches_oracle(R, Lg, k):
+    """Bit-exact selection (same binary32 entropies on both sides), ties
+    made frequent by rounding."""
+    _need_gpu()
+    rng = np.random.default_rng(R + Lg + k)
+    ent = np.round(rng.random((R, Lg)) * 6, 1).astype(np.float32)
+    sel = torch.empty(R, Lg, dtype=torch.uint8, device=DEV)
+    _binding.top_entropy(torch.as_tensor(ent, device=DEV), k, sel)
+    got = sel.cpu().numpy()
+    assert np.array_equal(got, oracle.top_entropy(ent, k))
+    assert np.all(got.sum(axis=1) == k)
+
+
+def test_forkgrpo_rollouts_and_objective():
+    """A ForkGRPO batch end to end: 2 prompts x 16 rollouts decoded with
+    Fork-dLLM (lambda = 0.8, candidates drawn at temperature 0.8), in
+    lock-step with the oracle; the fallback steps F_i, their positions
+    k_{i,t}, tokens and log q_old recorded from the oracle's trajectory and
+    compared with the GPU's; log q_new under a perturbed head by teacher
+    forcing; the objective on the GPU against the oracle's."""
+    _need_gpu()
+    cfg = synth.CONFIGS["grpo_small"]
+    G, temp, seed = 16, 0.8, 1234
+    B, L, BL = cfg.B, cfg.L, cfg.block_len
+    W = synth.weights(cfg)
+    Wb = host_bits(W)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    entries = []            # (step, b, k, token, lp_old oracle, lp_old gpu)
+    hs = []
+    excluded = 0
+    t = 0
+    while msk.any():
+        h = synth.hidden(cfg, t, W=W)
+        hs.append(h)
+        hb = host_bits(h)
+        g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, B, L, BL, cfg.tau, temperature=temp,
+                     seed=seed, counter=t)
+        act = []
+        for b in range(B):
+            m = [k for k in range(int(bs[b]), L) if msk[b * L + k]]
+            if m:
+                s = int(bs[b]) + ((m[0] - int(bs[b])) // BL) * BL
+                act += [b * L + k for k in range(s, min(s + BL, L))]
+        act = np.array(act, np.int64)
+        st = oracle.row_stats(hb, Wb, act)
+        sm = oracle.row_sample(hb, Wb, act, temp, seed, t)
+        ties = compare_sampled(g, st, sm, act, hb, Wb, cfg.d, temp, seed, t,
+                               __import__("harness").Report())
+        conf = np.full(cfg.M, np.nan)
+        cand = np.zeros(cfg.M, np.int32)
+        conf[act], cand[act] = sm["conf"], sm["cand"]
+        sel = oracle.select(conf, cand, tok, msk, bs, B, L, BL, float(np.float32(cfg.tau)))
+        logp_o = np.full(cfg.M, np.nan)
+        logp_o[act] = sm["logp"]
+        for b in range(B):
+            if sel[3][b] != 1:
+                continue
+            k = int(np.nonzero(msk[b * L:(b + 1) * L] & ~sel[1][b * L:(b + 1) * L])[0][0])
+            r = b * L + k
+            near = r in set(ties.tolist()) or abs(conf[r] - cfg.tau) < 1e-4
+            if near:
+                excluded += 1
+            else:
+                assert g.fallback[b] == 1 and g.commit_pos[b, 0] == k
+                assert g.tokens[r] == sel[0][r]
+                assert abs(g.logp[r] - logp_o[r]) <= STAT_TOL
+            entries.append((t, b, k, int(sel[0][r]), logp_o[r], float(g.logp[r])))
+        tok, msk, bs = sel[0], sel[1], sel[2]
+        t += 1
+        assert t <= cfg.G + 1
+    assert excluded <= max(2, len(entries) // 20)
+    # rollouts (one per sequence) with their fallback entries, CSR by rollout
+    entries.sort(key=lambda e: (e[1], e[0]))
+    counts = np.bincount([e[1] for e in entries], minlength=B)
+    assert counts.min() >= 1 and 0 < len(entries) < B * cfg.G
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    # the state x_{i,t} of each entry: the hidden row of its step
+    h_ent = torch.stack([hs[e[0]][e[1] * L + e[2]] for e in entries]).contiguous()
+    toks = np.array([e[3] for e in entries], np.int32)
+    gen = torch.Generator().manual_seed(77)
+    W_new = (W.float() + 0.2 * torch.randn(W.shape, generator=gen) / math.sqrt(cfg.d)).to(W.dtype)
+    ref_new = oracle.token_logprob(host_bits(h_ent), host_bits(W_new), np.arange(len(entries)), toks)
+    g_new = _logprob(h_ent.to(DEV), W_new.to(DEV), None, torch.as_tensor(toks, device=DEV))
+    assert np.all(np.abs(g_new["logp"] - ref_new["logp"]) <= STAT_TOL)
+    rewards = np.random.default_rng(5).integers(0, 2, B).astype(np.float32)
+    lp_old_o = np.array([e[4] for e in entries])
+    # the objective kernel on the oracle's binary32-rounded log-probabilities
+    lpn32, lpo32 = ref_new["logp"].astype(np.float32), lp_old_o.astype(np.float32)
+    g_obj = _objective(rewards, off, lpn32, lpo32, G, 0.2)
+    _compare_objective(g_obj, oracle.grpo_objective(rewards, off, lpn32, lpo32, G, 0.2))
+    # and end to end on the GPU's own log-probabilities: each log q is within
+    # STAT_TOL, so each log-ratio within 2 STAT_TOL, and each term within
+    # |A| max(rho, 1 + eps) (e^(2 STAT_TOL) - 1)
+    lp_old_g = np.array([e[5] for e in entries], np.float32)
+    g_e2e = _objective(rewards, off, g_new["logp"], lp_old_g, G, 0.2)
+    ref = oracle.grpo_objective(rewards, off, ref_new["logp"], lp_old_o, G, 0.2)
+    bound = np.abs(ref["adv"]).max() * max(ref["ratio"].max(), 1.2) * math.expm1(2 * STAT_TOL)
+    assert abs(g_e2e["J"] - ref["J"]) <= bound + OBJ_TOL
+    _say("ForkGRPO batch: %d steps, %d fallback entries (%d near-threshold), J gpu %.6f oracle %.6f"
+         % (t, len(entries), excluded, g_e2e["J"], ref["J"]))
