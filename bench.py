@@ -17,7 +17,9 @@ times the same decode with the LM head restricted to each sequence's active
 block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload; `drawn_candidates`
 times both modes with candidates drawn at sampling temperature 0.8;
 `forkgrpo_likelihood` times one ForkGRPO batch of 4096 teacher-forced
-log-probabilities plus its objective.
+log-probabilities plus its objective; `selection` gives the unmasking
+rule's latency at the real shapes and its HBM bandwidth on a sweep of large
+batches.
 """
 import argparse
 import ctypes
@@ -160,6 +162,64 @@ def grpo_likelihood(args, hip, W, h, dev):
                          "kernel": "gemm_stats_bf16_target_kernel (teacher-forced LM head)"}}
 
 
+SEL_BYTES_PER_SEQ = 4 + 32 + 32 * 4 + 4 + (4 + 1 + 4 + 4)
+
+
+def selection(args, dev):
+    """The unmasking rule alone (fork_select).  At the real shapes it moves a
+    few KB and is bound by launch latency: report its latency.  Its
+    bandwidth is shown on a sweep of large batches (2^14..2^20 sequences,
+    one block of 32 positions each, confidences at most 0.03 as at the
+    LLaDA-8B shape, so every step is a fallback step committing one
+    position): algorithmic bytes per sequence = block start, the block's 32
+    mask bytes and 32 confidences read, the committed candidate read, and
+    token, mask byte, fallback flag and block start written."""
+    import torch
+
+    from paper_2609_39859_amd import _binding
+    out = {"latency_us": {}, "sweep": []}
+
+    def run(B, L, BL, reps, warmup):
+        gen = torch.Generator(device=dev).manual_seed(B + L)
+        M = B * L
+        conf = torch.rand(M, generator=gen, device=dev) * 0.03
+        am = torch.randint(0, 126464, (M,), generator=gen, device=dev, dtype=torch.int32)
+        tok = torch.full((M,), -1, dtype=torch.int32, device=dev)
+        msk = torch.ones(M, dtype=torch.uint8, device=dev)
+        bs = torch.zeros(B, dtype=torch.int32, device=dev)
+        fb = torch.empty(B, dtype=torch.int32, device=dev)
+        for _ in range(warmup):
+            _binding.select(conf, am, tok, msk, bs, BL, 0.9, fb, B=B, L=L)
+        torch.cuda.synchronize()
+        # the timed launches replay as one HIP graph, so host launch
+        # overhead does not separate them (the call allocates nothing)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(reps):
+                _binding.select(conf, am, tok, msk, bs, BL, 0.9, fb, B=B, L=L)
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record()
+        graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        assert int((fb == 1).sum().item()) == B
+        assert int(msk.view(B, L)[:, :warmup + reps].sum().item()) == 0
+        return start.elapsed_time(stop) * 1e3 / reps
+
+    for name, B, L, BL in (("llada8b", 8, 512, 32), ("rollout", 64, 384, 32),
+                           ("long", 2, 2048, 64)):
+        out["latency_us"][name] = run(B, L, BL, 20, 3)
+    for B in (1 << 14, 1 << 17, 1 << 20):
+        us = run(B, 32, 32, 20, 3)   # 23 steps commit positions 0..22 of 32
+        gbs = SEL_BYTES_PER_SEQ * B / (us * 1e-6) / 1e9
+        out["sweep"].append({"B": B, "L": 32, "block_len": 32, "us": us, "GB_s": gbs,
+                             "frac_hbm": gbs / PEAK_HBM_GBS,
+                             "bytes_per_seq": SEL_BYTES_PER_SEQ})
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,6 +234,8 @@ def main():
                     help="skip the extra timings with candidates drawn at temperature 0.8")
     ap.add_argument("--no-grpo", action="store_true",
                     help="skip the timing of the ForkGRPO likelihood batch")
+    ap.add_argument("--no-selection", action="store_true",
+                    help="skip the selection latency and bandwidth sweep")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -341,6 +403,9 @@ def main():
         out["drawn_candidates"] = drawn
     if not args.no_grpo:
         out["forkgrpo_likelihood"] = grpo_likelihood(args, hip, W, hs[0], dev)
+    if not args.no_selection:
+        print("bench: selection latency and bandwidth sweep", file=sys.stderr, flush=True)
+        out["selection"] = selection(args, dev)
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)

@@ -191,6 +191,31 @@ int fork_step_ex(const fork_step_args* args);
    are invalid. */
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
 
+/* The unmasking rule alone (Algorithm 2; the `rule` variants of
+   fork_step_args), applied in place to B sequences from per-position
+   confidences and candidates computed elsewhere: exactly the selection stage
+   of fork_step_ex, with the same arguments, semantics and outputs
+   (out_fallback per sequence; out_ncommit and out_commit_pos optional).
+   entropy ([B*L]) is needed by FORK_RULE_MAXENT, uniform ([B]) by
+   FORK_RULE_RANDOM.  Returns FORK_OK, FORK_EINVAL or FORK_EHIP. */
+typedef struct fork_select_args {
+  const float* conf;       /* [B*L] confidence of each position's candidate    */
+  const float* entropy;    /* [B*L] or NULL                                    */
+  const float* uniform;    /* [B] or NULL                                      */
+  const int32_t* argmax;   /* [B*L] candidate token of each position           */
+  int32_t* tokens;         /* [B*L] in/out                                     */
+  uint8_t* mask;           /* [B*L] in/out                                     */
+  int32_t* block_start;    /* [B]   in/out                                     */
+  int32_t* out_fallback;   /* [B]                                              */
+  int32_t* out_ncommit;    /* [B] or NULL                                      */
+  int32_t* out_commit_pos; /* [B*block_len] or NULL                            */
+  int32_t B, L, block_len;
+  float tau;
+  int32_t rule;
+  void* stream;
+} fork_select_args;
+int fork_select(const fork_select_args* args);
+
 /* ------------------------------------------------------------ ForkGRPO
  *
  * Section 3.2 of the paper trains on the fallback steps of Fork-dLLM

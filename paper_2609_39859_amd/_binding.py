@@ -74,6 +74,16 @@ class ForkGrpoArgs(ctypes.Structure):
     ]
 
 
+class ForkSelectArgs(ctypes.Structure):
+    _fields_ = [
+        ("conf", _P), ("entropy", _P), ("uniform", _P), ("argmax", _P),
+        ("tokens", _P), ("mask", _P), ("block_start", _P),
+        ("out_fallback", _P), ("out_ncommit", _P), ("out_commit_pos", _P),
+        ("B", _I32), ("L", _I32), ("block_len", _I32), ("tau", ctypes.c_float),
+        ("rule", _I32), ("stream", _P),
+    ]
+
+
 class ForkError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__("fork_step failed (%d): %s" % (code, msg))
@@ -113,6 +123,8 @@ def lib():
         L.fork_logprob_workspace_bytes.argtypes = [_I32, _I32]
         L.fork_grpo_objective.restype = ctypes.c_int
         L.fork_grpo_objective.argtypes = [ctypes.POINTER(ForkGrpoArgs)]
+        L.fork_select.restype = ctypes.c_int
+        L.fork_select.argtypes = [ctypes.POINTER(ForkSelectArgs)]
         L.fork_top_entropy.restype = ctypes.c_int
         L.fork_top_entropy.argtypes = [_P, _I32, _I32, _I32, _P, _P]
         _lib = L
@@ -304,6 +316,32 @@ def top_entropy(entropy: torch.Tensor, k: int, out_sel: torch.Tensor, stream=Non
     e = _check(entropy, "entropy", torch.float32, R * Lg, device)
     o = _check(out_sel, "out_sel", torch.uint8, R * Lg, device)
     _raise_on(lib().fork_top_entropy(e, R, Lg, int(k), o, _stream_handle(stream, device)))
+
+
+def select(conf: torch.Tensor, argmax: torch.Tensor, tokens: torch.Tensor, mask: torch.Tensor,
+           block_start: torch.Tensor, block_len: int, tau: float, out_fallback: torch.Tensor, *,
+           B: int, L: int, rule: int = FORK_RULE_LEFTMOST, entropy=None, uniform=None,
+           out_ncommit=None, out_commit_pos=None, stream=None) -> None:
+    """fork_select of the C ABI: the unmasking rule alone, in place."""
+    device = conf.device
+    if device.type != "cuda":
+        raise ValueError("fork_select runs on the GPU")
+    M = B * L
+    a = ForkSelectArgs()
+    a.conf = _check(conf, "conf", torch.float32, M, device)
+    a.entropy = _opt(entropy, "entropy", torch.float32, M, device)
+    a.uniform = _opt(uniform, "uniform", torch.float32, B, device)
+    a.argmax = _check(argmax, "argmax", torch.int32, M, device)
+    a.tokens = _check(tokens, "tokens", torch.int32, M, device)
+    a.mask = _check(mask, "mask", torch.uint8, M, device)
+    a.block_start = _check(block_start, "block_start", torch.int32, B, device)
+    a.out_fallback = _check(out_fallback, "out_fallback", torch.int32, B, device)
+    a.out_ncommit = _opt(out_ncommit, "out_ncommit", torch.int32, B, device)
+    a.out_commit_pos = _opt(out_commit_pos, "out_commit_pos", torch.int32, B * int(block_len),
+                            device)
+    a.B, a.L, a.block_len, a.tau, a.rule = B, L, int(block_len), float(tau), int(rule)
+    a.stream = _stream_handle(stream, device)
+    _raise_on(lib().fork_select(ctypes.byref(a)))
 
 
 def logprob_workspace_bytes(n: int, V: int) -> int:

@@ -303,6 +303,30 @@ int fork_logprob(const fork_logprob_args* a) {
   return FORK_OK;
 }
 
+int fork_select(const fork_select_args* a) {
+  if (!a) return fail(FORK_EINVAL, "args is NULL");
+  if (!a->conf || !a->argmax || !a->tokens || !a->mask || !a->block_start || !a->out_fallback)
+    return fail(FORK_EINVAL, "a required pointer is NULL");
+  if (a->B <= 0 || a->L <= 0) return fail(FORK_EINVAL, "sizes must be positive (B=%d L=%d)", a->B, a->L);
+  if ((long long)a->B * a->L > 0x7fffffffLL)
+    return fail(FORK_EINVAL, "B*L = %lld does not fit int32", (long long)a->B * a->L);
+  if (a->block_len <= 0 || a->block_len > a->L)
+    return fail(FORK_EINVAL, "block_len=%d must lie in [1, L=%d]", a->block_len, a->L);
+  if (!isfinite(a->tau)) return fail(FORK_EINVAL, "tau must be finite");
+  if (a->rule < FORK_RULE_LEFTMOST || a->rule > FORK_RULE_RANDOM)
+    return fail(FORK_EINVAL, "unknown fallback rule %d", a->rule);
+  if (a->rule == FORK_RULE_RANDOM && !a->uniform)
+    return fail(FORK_EINVAL, "FORK_RULE_RANDOM needs uniform");
+  if (a->rule == FORK_RULE_MAXENT && !a->entropy)
+    return fail(FORK_EINVAL, "FORK_RULE_MAXENT needs entropy");
+  hipError_t e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->conf,
+                                     a->entropy, a->uniform, a->argmax, a->tokens, a->mask,
+                                     a->block_start, a->out_fallback, a->out_ncommit,
+                                     a->out_commit_pos, static_cast<hipStream_t>(a->stream));
+  if (e != hipSuccess) return fail(FORK_EHIP, "select launch: %s", hipGetErrorString(e));
+  return FORK_OK;
+}
+
 int fork_grpo_objective(const fork_grpo_args* a) {
   if (!a) return fail(FORK_EINVAL, "args is NULL");
   if (a->n_groups < 0 || a->G <= 0 || a->n < 0)

@@ -79,6 +79,11 @@ hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
 
 // Unmasking rule per sequence, in place.  ncommit / commit_pos may be null;
 // entropy is read by the highest-entropy rule, uniform by the random rule.
+// Batches of at least kLaneSelectMinB sequences with blocks of at most
+// kLaneSelectMaxBL positions run one lane per sequence, others one wave per
+// sequence; both give the same results.
+constexpr int kLaneSelectMinB = 4096;
+constexpr int kLaneSelectMaxBL = 64;
 hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          const float* conf, const float* entropy, const float* uniform,
                          const int32_t* argmax,

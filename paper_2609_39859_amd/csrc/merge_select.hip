@@ -251,6 +251,170 @@ __global__ __launch_bounds__(64) void select_kernel(
   }
 }
 
+// The same rule with one lane per sequence, for large batches of short
+// blocks: each lane walks its block position by position, so a wave keeps
+// the loads of 64 sequences in flight instead of one (the wave-per-sequence
+// kernel is latency-bound once B reaches thousands).  Decisions are those of
+// select_kernel: binary32 threshold test, lowest position on ties.
+__global__ __launch_bounds__(256) void select_lanes_kernel(
+    int B, int L, int BL, float tau, int rule, const float* __restrict__ conf,
+    const float* __restrict__ entropy, const float* __restrict__ uniform,
+    const int32_t* __restrict__ argmax, int32_t* __restrict__ tokens,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ block_start,
+    int32_t* __restrict__ fallback, int32_t* __restrict__ ncommit,
+    int32_t* __restrict__ commit_pos) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  const size_t base = (size_t)b * L;
+  int32_t* my_commits = commit_pos ? commit_pos + (size_t)b * BL : nullptr;
+  int s = block_start[b];
+  if (s < 0 || s > L) {
+    fallback[b] = -2;
+    if (ncommit) ncommit[b] = 0;
+    if (my_commits)
+      for (int i = 0; i < BL; ++i) my_commits[i] = -1;
+    return;
+  }
+  // Blocks of at most 32 positions whose 32 entries from s stay in the row
+  // and start 16-byte aligned: mask and confidences come in with wide loads
+  // issued together and the decision is taken on a bitmask in registers.
+  if (rule != kMaxEnt && BL <= 32 && s + 32 <= L &&
+      ((reinterpret_cast<uintptr_t>(mask + base + s) | reinterpret_cast<uintptr_t>(conf + base + s)) &
+       15) == 0) {
+    const int cnt = min(BL, L - s);
+    const uint4 mv0 = *reinterpret_cast<const uint4*>(mask + base + s);
+    const uint4 mv1 = *reinterpret_cast<const uint4*>(mask + base + s + 16);
+    float c[32];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float4 v = *reinterpret_cast<const float4*>(conf + base + s + 4 * q);
+      c[4 * q] = v.x;
+      c[4 * q + 1] = v.y;
+      c[4 * q + 2] = v.z;
+      c[4 * q + 3] = v.w;
+    }
+    const uint32_t mw[8] = {mv0.x, mv0.y, mv0.z, mv0.w, mv1.x, mv1.y, mv1.z, mv1.w};
+    uint32_t mbits = 0, pbits = 0;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const bool m = i < cnt && ((mw[i >> 2] >> (8 * (i & 3))) & 0xffu) != 0;
+      mbits |= (uint32_t)m << i;
+      pbits |= (uint32_t)(m && c[i] > tau) << i;
+    }
+    if (mbits != 0) {  // the block at s is the active block
+      const bool fb = pbits == 0;
+      uint32_t commit = pbits;
+      if (fb) {
+        int pick = 0;
+        if (rule == kLeftmost) {
+          pick = __ffs(mbits) - 1;
+        } else if (rule == kRandom) {
+          const int n = __popc(mbits);
+          int j = (int)(uniform[b] * (float)n);
+          j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
+          uint32_t rest = mbits;
+          for (int t = 0; t < j; ++t) rest &= rest - 1;  // drop the j lowest
+          pick = __ffs(rest) - 1;
+        } else {
+          const bool lowest = rule == kMinConf;
+          float best = 0.f;
+          int bi = -1;
+#pragma unroll
+          for (int i = 0; i < 32; ++i)
+            if (((mbits >> i) & 1u) && (bi < 0 || (lowest ? c[i] < best : c[i] > best))) {
+              best = c[i];
+              bi = i;
+            }
+          pick = bi;
+        }
+        commit = 1u << pick;
+      }
+      int written = 0;
+      for (uint32_t rest = commit; rest; rest &= rest - 1) {
+        const int k = s + __ffs(rest) - 1;
+        tokens[base + k] = argmax[base + k];
+        mask[base + k] = 0;
+        if (my_commits) my_commits[written] = k;
+        ++written;
+      }
+      if (my_commits)
+        for (int i = written; i < BL; ++i) my_commits[i] = -1;
+      fallback[b] = fb ? 1 : 0;
+      block_start[b] = s;
+      if (ncommit) ncommit[b] = written;
+      return;
+    }
+    s += BL;  // nothing masked there: continue the skip-forward below
+  }
+  // skip forward to the first block holding a masked position
+  bool found = false;
+  while (s < L) {
+    const int e = min(s + BL, L);
+    for (int k = s; k < e && !found; ++k) found = mask[base + k] != 0;
+    if (found) break;
+    s += BL;
+  }
+  if (!found) {
+    fallback[b] = -1;
+    if (ncommit) ncommit[b] = 0;
+    if (my_commits)
+      for (int i = 0; i < BL; ++i) my_commits[i] = -1;
+    return;
+  }
+  const int e = min(s + BL, L);
+  // threshold count, masked count, leftmost masked, extreme of the key
+  const float* key = rule == kMaxEnt ? entropy : conf;
+  const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
+  const bool lowest = rule == kMinConf;
+  int npass = 0, n = 0, first = -1, bi = -1;
+  float best = 0.f;
+  for (int k = s; k < e; ++k) {
+    if (!mask[base + k]) continue;
+    ++n;
+    if (first < 0) first = k;
+    if (conf[base + k] > tau) ++npass;
+    if (extreme) {
+      const float v = key[base + k];
+      if (bi < 0 || (lowest ? v < best : v > best)) {
+        best = v;
+        bi = k;
+      }
+    }
+  }
+  const bool fb = npass == 0;
+  int pick = -1;
+  if (fb) {
+    if (rule == kLeftmost) {
+      pick = first;
+    } else if (rule == kRandom) {
+      int j = (int)(uniform[b] * (float)n);
+      j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
+      for (int k = s; k < e; ++k)
+        if (mask[base + k] && j-- == 0) {
+          pick = k;
+          break;
+        }
+    } else {
+      pick = bi;
+    }
+  }
+  int written = 0;
+  for (int k = s; k < e; ++k) {
+    if (!mask[base + k]) continue;
+    if (fb ? (k == pick) : (conf[base + k] > tau)) {
+      tokens[base + k] = argmax[base + k];
+      mask[base + k] = 0;
+      if (my_commits) my_commits[written] = k;
+      ++written;
+    }
+  }
+  if (my_commits)
+    for (int i = written; i < BL; ++i) my_commits[i] = -1;
+  fallback[b] = fb ? 1 : 0;
+  block_start[b] = s;
+  if (ncommit) ncommit[b] = written;
+}
+
 // Active block of each sequence (first block from block_start holding a
 // masked position, as in the selection) expanded to its rows.
 __global__ __launch_bounds__(64) void active_rows_kernel(int L, int BL,
@@ -314,9 +478,14 @@ hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          const int32_t* argmax, int32_t* tokens, uint8_t* mask,
                          int32_t* block_start, int32_t* fallback, int32_t* ncommit,
                          int32_t* commit_pos, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)B), dim3(64), 0, stream, L,
-                     block_len, tau, rule, conf, entropy, uniform, argmax, tokens, mask,
-                     block_start, fallback, ncommit, commit_pos);
+  if (B >= kLaneSelectMinB && block_len <= kLaneSelectMaxBL)
+    hipLaunchKernelGGL(select_lanes_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
+                       stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
+                       tokens, mask, block_start, fallback, ncommit, commit_pos);
+  else
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)B), dim3(64), 0, stream, L,
+                       block_len, tau, rule, conf, entropy, uniform, argmax, tokens, mask,
+                       block_start, fallback, ncommit, commit_pos);
   return hipGetLastError();
 }
 

@@ -197,3 +197,26 @@ def test_grpo_bad_arguments_rejected_on_host(kw):
 def test_top_entropy_bad_arguments_rejected_on_host(R, Lg, k, ptr, code):
     L = _binding.lib()
     assert L.fork_top_entropy(ptr, R, Lg, k, ptr, None) == code
+
+
+def _sel_args(**kw):
+    a = _binding.ForkSelectArgs()
+    good = dict(conf=16, argmax=32, tokens=48, mask=64, block_start=80, out_fallback=96,
+                B=2, L=8, block_len=4, tau=0.9, rule=0)
+    good.update(kw)
+    for k, v in good.items():
+        assert hasattr(a, k)
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("kw", [
+    dict(conf=0), dict(argmax=0), dict(tokens=0), dict(mask=0), dict(block_start=0),
+    dict(out_fallback=0), dict(B=0), dict(L=-1), dict(block_len=0), dict(block_len=9),
+    dict(tau=float("nan")), dict(rule=5), dict(rule=4), dict(rule=3),
+    dict(B=1 << 16, L=1 << 16),
+])
+def test_select_bad_arguments_rejected_on_host(kw):
+    L = _binding.lib()
+    assert L.fork_select(ctypes.byref(_sel_args(**kw))) == _binding.FORK_EINVAL
+    assert L.fork_last_error().decode() != ""

@@ -1,0 +1,105 @@
+"""GPU parity of the unmasking rule on its own (fork_select, Algorithm 2 and
+the fallback rules of Algorithm 1 and Section 4.1): both kernel paths (one
+wave per sequence, and one lane per sequence for large batches of short
+blocks) against the oracle, bit for bit (both sides decide on the same
+binary32 confidences)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39859_amd import _binding
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _state(B, L, V, seed):
+    rng = np.random.default_rng(seed)
+    M = B * L
+    conf = rng.random(M).astype(np.float32)
+    conf[rng.random(M) < 0.1] = np.float32(0.9)           # values on the threshold
+    ent = np.round(rng.random(M) * 4, 2).astype(np.float32)  # frequent ties
+    am = rng.integers(0, V, M).astype(np.int32)
+    msk = (rng.random(M) < 0.5).astype(np.uint8)
+    tok = np.where(msk, -1, rng.integers(0, V, M)).astype(np.int32)
+    bs = rng.integers(0, L + 1, B).astype(np.int32)
+    msk[(B - 1) * L:] = 0                                  # an idle sequence
+    uni = rng.random(B).astype(np.float32)
+    return conf, ent, am, tok, msk, bs, uni
+
+
+def _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule):
+    t = lambda x: torch.as_tensor(np.ascontiguousarray(x), device=DEV)
+    tok_d, msk_d, bs_d = t(tok.copy()), t(msk.copy()), t(bs.copy())
+    fb = torch.full((B,), -9, dtype=torch.int32, device=DEV)
+    nc = torch.full((B,), -9, dtype=torch.int32, device=DEV)
+    cp = torch.full((B * BL,), -9, dtype=torch.int32, device=DEV)
+    _binding.select(t(conf), t(am), tok_d, msk_d, bs_d, BL, tau, fb, B=B, L=L, rule=rule,
+                    entropy=t(ent), uniform=t(uni), out_ncommit=nc, out_commit_pos=cp)
+    torch.cuda.synchronize()
+    return (tok_d.cpu().numpy(), msk_d.cpu().numpy(), bs_d.cpu().numpy(), fb.cpu().numpy(),
+            nc.cpu().numpy(), cp.cpu().numpy().reshape(B, BL))
+
+
+SHAPES = [
+    # B, L, block_len   (B >= 4096 with block_len <= 64 takes the lane path)
+    (5, 61, 7), (37, 300, 300), (4096, 40, 8), (5000, 64, 64), (4100, 33, 32),
+    (4096, 100, 65), (4097, 1, 1),
+    # lane path with 16-byte aligned rows and blocks <= 32 (wide loads)
+    (4096, 32, 32), (4096, 64, 16), (8192, 96, 32), (4096, 48, 8),
+]
+
+
+@pytest.mark.parametrize("B,L,BL", SHAPES)
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
+def test_select_matches_oracle(B, L, BL, rule):
+    _need_gpu()
+    conf, ent, am, tok, msk, bs, uni = _state(B, L, 1000, B * 31 + L + BL + rule)
+    for tau in (0.3, 0.9):
+        g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule)
+        o = oracle.select_ex(conf, am, tok, msk, bs, B, L, BL, float(np.float32(tau)), rule,
+                             entropy=ent, uniform=uni)
+        for k, (x, y) in enumerate(zip(g[:5], o)):
+            assert np.array_equal(x, y), ("tokens", "mask", "block_start", "fallback", "ncommit")[k]
+        # compacted commits: the positions the oracle unmasked, ascending
+        for b in range(B):
+            sl = slice(b * L, (b + 1) * L)
+            done = np.nonzero(msk[sl] & ~o[1][sl])[0]
+            assert np.array_equal(g[5][b, :done.size], done)
+            assert np.all(g[5][b, done.size:] == -1)
+
+
+def test_lane_and_wave_paths_agree():
+    """The first sequences of a large batch (lane path) and the same
+    sequences run as a small batch (wave path) give identical results."""
+    _need_gpu()
+    B, L, BL = 4096, 64, 32
+    conf, ent, am, tok, msk, bs, uni = _state(B, L, 500, 7)
+    for rule in range(5):
+        big = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.5, rule)
+        n = 64
+        small = _run(conf[:n * L], ent[:n * L], am[:n * L], tok[:n * L], msk[:n * L], bs[:n],
+                     uni[:n], n, L, BL, 0.5, rule)
+        for x, y in zip(big, small):
+            assert np.array_equal(x.reshape(-1)[:y.size], y.reshape(-1))
+
+
+@pytest.mark.parametrize("B", [3, 4096])
+def test_bad_block_start_reported_in_data_on_both_paths(B):
+    _need_gpu()
+    L, BL = 16, 4
+    conf, ent, am, tok, msk, bs, uni = _state(B, L, 100, 3)
+    msk[:] = 1
+    bs[:] = 0
+    bs[0], bs[1] = -1, L + 1
+    bs[2] = L                           # nothing at or after the start: idle
+    g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.5, 0)
+    assert g[3][:3].tolist() == [-2, -2, -1]
+    assert np.all(g[1][:3 * L] == 1) and np.all(g[4][:3] == 0) and np.all(g[5][:3] == -1)
