@@ -19,7 +19,8 @@ times both modes with candidates drawn at sampling temperature 0.8;
 `forkgrpo_likelihood` times one ForkGRPO batch of 4096 teacher-forced
 log-probabilities plus its objective; `selection` gives the unmasking
 rule's latency at the real shapes and its HBM bandwidth on a sweep of large
-batches.
+batches; `measured_peaks` gives this GPU's achievable MFMA and HBM rates
+(probe kernels), and the rooflines also quote fractions of those.
 """
 import argparse
 import ctypes
@@ -163,6 +164,49 @@ def grpo_likelihood(args, hip, W, h, dev):
 
 
 SEL_BYTES_PER_SEQ = 4 + 32 + 32 * 4 + 4 + (4 + 1 + 4 + 4)
+PROBE_LIB = os.path.join(ROOT, "paper_2609_39859_amd", "libforkprobe.so")
+
+
+def measured_peaks(dev):
+    """The achievable rates of this GPU: dense bf16 MFMA from a kernel that
+    only issues independent MFMAs on register operands, HBM from a streaming
+    copy of 2 x 1 GiB (read + write)."""
+    import torch
+    lib = ctypes.CDLL(PROBE_LIB)
+    lib.fork_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fork_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                    ctypes.c_int, ctypes.c_void_p]
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    blocks, iters = 7904, 256      # the LM head's grid and K/16 at the LLaDA-8B shape
+    out = torch.empty(blocks * 512, device=dev)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    assert lib.fork_probe_mfma(blocks, 100, out.data_ptr(), stream) == 0
+    torch.cuda.synchronize()
+    start.record()
+    assert lib.fork_probe_mfma(blocks, iters, out.data_ptr(), stream) == 0
+    stop.record()
+    torch.cuda.synchronize()
+    mfma = blocks * 8.0 * iters * 8 * 32768 / (start.elapsed_time(stop) * 1e-3) / 1e12
+    n = (1 << 30) // 16
+    src = torch.ones(n * 16, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, 4096, stream) == 0
+    torch.cuda.synchronize()
+    reps = 5
+    start.record()
+    for _ in range(reps):
+        assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, 4096, stream) == 0
+    stop.record()
+    torch.cuda.synchronize()
+    assert bool(dst[-1] == 1)
+    hbm = 2.0 * (1 << 30) * reps / (start.elapsed_time(stop) * 1e-3) / 1e9
+    del src, dst
+    return {"mfma_bf16_TFLOP_s": mfma, "hbm_copy_GB_s": hbm,
+            "how": "MFMA: 7904 workgroups x 8 waves x 256 rounds of 8 independent "
+                   "v_mfma_f32_32x32x16_bf16 on register operands (the flops of one LM-head "
+                   "launch); HBM: streaming copy of 1 GiB (4 x 16 B per thread per "
+                   "iteration), read + write counted, 5 repetitions"}
 
 
 def selection(args, dev):
@@ -236,6 +280,8 @@ def main():
                     help="skip the timing of the ForkGRPO likelihood batch")
     ap.add_argument("--no-selection", action="store_true",
                     help="skip the selection latency and bandwidth sweep")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measurement of the achievable MFMA and HBM rates")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -406,6 +452,20 @@ def main():
     if not args.no_selection:
         print("bench: selection latency and bandwidth sweep", file=sys.stderr, flush=True)
         out["selection"] = selection(args, dev)
+    if not args.no_peaks:
+        print("bench: measuring achievable MFMA and HBM rates", file=sys.stderr, flush=True)
+        pk = measured_peaks(dev)
+        out["measured_peaks"] = pk
+        rf = out["roofline"]
+        rf["measured_peak"] = pk["mfma_bf16_TFLOP_s"]
+        rf["frac_of_measured_peak"] = rf["achieved"] / pk["mfma_bf16_TFLOP_s"]
+        if "active_rows_mode" in out:
+            ar = out["active_rows_mode"]["roofline"]
+            ar["measured_peak"] = pk["hbm_copy_GB_s"]
+            ar["frac_of_measured_peak"] = ar["achieved"] / pk["hbm_copy_GB_s"]
+        if "selection" in out:
+            for x in out["selection"]["sweep"]:
+                x["frac_of_measured_hbm"] = x["GB_s"] / pk["hbm_copy_GB_s"]
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)

@@ -1,7 +1,8 @@
 """Build of the HIP library (libforkstep.so) for gfx950.
 
-``python -m paper_2609_39859_amd.build`` compiles every HIP source under
-csrc/ with hipcc into one shared library next to this file.  The compile
+``python -m paper_2609_39859_amd.build`` compiles the library's HIP sources
+under csrc/ with hipcc into libforkstep.so next to this file, and the
+benchmark's peak probes (csrc/peak_probe.hip) into libforkprobe.so.  The compile
 disables packed-fp32 instruction selection (the -packed-fp32-ops target
 feature); hipcc's host pass warns that it does not know the feature, which is
 harmless.
@@ -18,6 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libforkstep.so")
 SOURCES = ["gemm_stats.hip", "merge_select.hip", "grpo.hip", "fork_abi.hip"]
+PROBE_LIB = os.path.join(HERE, "libforkprobe.so")
+PROBE_SOURCES = ["peak_probe.hip"]
 ARCH = "gfx950"
 
 
@@ -35,12 +38,18 @@ def compile_flags():
 
 
 def build(verbose: bool = False) -> str:
-    """Compile and link libforkstep.so; returns its path."""
+    """Compile and link libforkstep.so and libforkprobe.so; returns the
+    path of libforkstep.so."""
+    _build_lib(PROBE_LIB, PROBE_SOURCES, verbose)
+    return _build_lib(LIB, SOURCES, verbose)
+
+
+def _build_lib(lib_path: str, sources, verbose: bool) -> str:
     objs = []
     builddir = os.path.join(HERE, "_build")
     os.makedirs(builddir, exist_ok=True)
     procs = []
-    for src in SOURCES:
+    for src in sources:
         obj = os.path.join(builddir, os.path.splitext(src)[0] + ".o")
         cmd = [hipcc()] + compile_flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
@@ -59,13 +68,13 @@ def build(verbose: bool = False) -> str:
             failed.append(src)
     if failed:
         raise RuntimeError("hipcc failed for %s" % ", ".join(failed))
-    tmp = LIB + ".tmp%d" % os.getpid()
+    tmp = lib_path + ".tmp%d" % os.getpid()
     cmd = [hipcc(), "-shared", "-fPIC", "--offload-arch=%s" % ARCH, "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -1,0 +1,80 @@
+// Measurement probes for the benchmark (not part of the Fork-dLLM library):
+// the achievable dense bf16 MFMA rate and HBM streaming rate of the GPU the
+// benchmark runs on, against which its roofline fractions are also quoted.
+// Built into its own small library (libforkprobe.so), loaded by bench.py.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Each wave issues `iters` rounds of 8 independent 32x32x16 bf16 MFMAs on
+// register-resident operands (no memory traffic inside the loop); 512-thread
+// workgroups put two waves on each SIMD, as the LM-head kernel does.
+__global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (float)(lane + i));
+    b[i] = (__bf16)(0.002f * (float)(lane - i));
+  }
+  f32x16 acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[t], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[t][e];
+  out[blockIdx.x * 512 + threadIdx.x] = s;
+}
+
+// Streaming copy: each thread moves four 16-byte elements per iteration
+// (consecutive threads on consecutive elements), grid-stride.
+__global__ __launch_bounds__(256) void stream_copy_kernel(const uint4* __restrict__ src,
+                                                          uint4* __restrict__ dst, size_t n) {
+  const size_t stride = (size_t)gridDim.x * 1024;
+  for (size_t i = (size_t)blockIdx.x * 1024 + threadIdx.x; i < n; i += stride) {
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (i + 256 * j < n) v[j] = src[i + 256 * j];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (i + 256 * j < n) dst[i + 256 * j] = v[j];
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Launches the MFMA probe: `blocks` workgroups of 512 threads, `iters`
+// rounds each; out must hold blocks * 512 floats.  Returns a hipError_t.
+// Dense bf16 flops of one launch = blocks * 8 waves * iters * 8 * 32768.
+int fork_probe_mfma(int blocks, int iters, float* out, void* stream) {
+  hipLaunchKernelGGL(mfma_peak_kernel, dim3((unsigned)blocks), dim3(512), 0,
+                     static_cast<hipStream_t>(stream), iters, out);
+  return (int)hipGetLastError();
+}
+
+// Launches the copy probe on n 16-byte elements (src and dst 16-byte
+// aligned, n * 16 bytes each).  Returns a hipError_t.
+int fork_probe_copy(const void* src, void* dst, size_t n, int blocks, void* stream) {
+  hipLaunchKernelGGL(stream_copy_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const uint4*>(src),
+                     static_cast<uint4*>(dst), n);
+  return (int)hipGetLastError();
+}
+
+}  // extern "C"
