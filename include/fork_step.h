@@ -119,9 +119,11 @@ enum {
  * dtype        FORK_BF16 or FORK_F32.
  * stream       hipStream_t to enqueue on (NULL = default stream).
  *
- * Returns FORK_OK or a negative FORK_E* code.  Uses the library-managed
- * workspace of the current device (grown on demand with hipMalloc, which may
- * synchronise the device; fork_release frees it).
+ * Returns FORK_OK or a negative FORK_E* code (FORK_EUNSUPPORTED also when
+ * the launch grid would exceed 2^32 work-items, i.e. when
+ * ceil(positions/256) * ceil(V/256) * 512 >= 2^32; split such batches).
+ * Uses the library-managed workspace of the current device (grown on demand
+ * with hipMalloc, which may synchronise the device; fork_release frees it).
  */
 int fork_step(const void* hidden, const void* W_head, int32_t* tokens,
               uint8_t* mask, int32_t* block_start, int32_t block_len,
@@ -176,7 +178,7 @@ typedef struct fork_step_args {
      such a position are q(cand) and log q(cand) of the untempered q (the
      confidence of Algorithm 2); out_entropy and out_lse are unchanged.
      Other positions keep the greedy candidate and its statistics.  Draws do
-     not depend on rows_mode.  Must be finite and >= 0 (FORK_EINVAL). */
+     not depend on rows_mode.  Must be 0 or in [1e-30, inf) (FORK_EINVAL). */
   float sample_temperature;
   uint32_t sample_counter; /* per-step counter of the draws (e.g. step index) */
   uint64_t sample_seed;    /* key of the draws                                 */

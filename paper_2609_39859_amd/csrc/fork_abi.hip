@@ -92,6 +92,17 @@ int get_workspace(size_t need, void** out) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Smallest positive sampling temperature: below it 1/tau overflows the
+// Gumbel keys.
+constexpr float kMinTemperature = 1e-30f;
+
+// The LM-head launch has one 512-thread workgroup per (vocabulary tile,
+// position tile); its work-item count must stay below 2^32.
+bool grid_fits(long long positions, int V) {
+  const long long tiles = (long long)fork::num_vocab_tiles(V) * ((positions + fork::kTileP - 1) / fork::kTileP);
+  return tiles * 512 < (1LL << 32);
+}
+
 int validate(const fork_step_args* a) {
   if (!a) return fail(FORK_EINVAL, "args is NULL");
   if (!a->hidden || !a->W_head || !a->tokens || !a->mask || !a->block_start || !a->out_conf ||
@@ -125,6 +136,12 @@ int validate(const fork_step_args* a) {
     return fail(FORK_EUNSUPPORTED, "FORK_ROWS_ACTIVE needs B*L*d*element_size < 2^31");
   if (!(a->sample_temperature >= 0.0f) || !isfinite(a->sample_temperature))
     return fail(FORK_EINVAL, "sample_temperature must be finite and >= 0");
+  if (a->sample_temperature > 0.0f && a->sample_temperature < kMinTemperature)
+    return fail(FORK_EINVAL, "sample_temperature must be 0 or at least %g", (double)kMinTemperature);
+  const int positions = a->rows_mode == FORK_ROWS_ACTIVE ? a->B * a->block_len : a->B * a->L;
+  if (!grid_fits(positions, a->V))
+    return fail(FORK_EUNSUPPORTED, "%d positions x V=%d exceed one launch grid; split the batch",
+                positions, a->V);
   return FORK_OK;
 }
 
@@ -266,6 +283,9 @@ int fork_logprob(const fork_logprob_args* a) {
     return fail(FORK_EUNSUPPORTED, "d=%d exceeds the supported maximum %d", a->d, kMaxD);
   if (a->rows && (long long)a->M * a->d * (a->dtype == FORK_BF16 ? 2 : 4) >= (1LL << 31))
     return fail(FORK_EUNSUPPORTED, "gathered rows need M*d*element_size < 2^31");
+  if (!grid_fits(a->n, a->V))
+    return fail(FORK_EUNSUPPORTED, "n=%d entries x V=%d exceed one launch grid; split the batch",
+                a->n, a->V);
   if (!aligned16(a->hidden) || !aligned16(a->W_head))
     return fail(FORK_EINVAL, "hidden and W_head must be 16-byte aligned");
   size_t zt_off, total;

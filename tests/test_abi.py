@@ -84,6 +84,8 @@ def _args(**kw):
     (dict(sample_temperature=float("nan")), _binding.FORK_EINVAL),
     (dict(sample_temperature=float("inf")), _binding.FORK_EINVAL),
     (dict(rows_mode=1, B=64, L=2048, d=8192), _binding.FORK_EUNSUPPORTED),
+    (dict(sample_temperature=1e-35), _binding.FORK_EINVAL),
+    (dict(B=1 << 14, L=1 << 10, block_len=4, V=126464), _binding.FORK_EUNSUPPORTED),
     (dict(rule=4), _binding.FORK_EINVAL),          # random rule without uniforms
     (dict(d=12), _binding.FORK_EUNSUPPORTED),
     (dict(d=6, dtype=_binding.FORK_F32), _binding.FORK_EUNSUPPORTED),
@@ -153,6 +155,7 @@ def _lp_args(**kw):
     (dict(rows=0, n=9), _binding.FORK_EINVAL),        # n > M without a row list
     (dict(d=12), _binding.FORK_EUNSUPPORTED),
     (dict(M=1 << 20, d=2048), _binding.FORK_EUNSUPPORTED),  # gathered rows past 2^31 bytes
+    (dict(rows=0, n=1 << 24, M=1 << 24, V=126464), _binding.FORK_EUNSUPPORTED),  # grid
     (dict(hidden=18), _binding.FORK_EINVAL),
     (dict(workspace=256, workspace_bytes=10), _binding.FORK_EINVAL),
 ])
