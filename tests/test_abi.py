@@ -223,3 +223,21 @@ def test_select_bad_arguments_rejected_on_host(kw):
     L = _binding.lib()
     assert L.fork_select(ctypes.byref(_sel_args(**kw))) == _binding.FORK_EINVAL
     assert L.fork_last_error().decode() != ""
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No CPU or PyTorch fallback: with the library missing, the first call
+    raises and says how to build it."""
+    import subprocess
+    import sys
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "from paper_2609_39859_amd import _binding\n"
+        "_binding.LIB_PATH = %r\n"
+        "try:\n"
+        "    _binding.lib()\n"
+        "except RuntimeError as e:\n"
+        "    assert 'not built' in str(e), e\n"
+        "    print('raised')\n" % (ROOT, str(tmp_path / "absent.so")))
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0 and out.stdout.strip() == "raised", out.stderr

@@ -404,6 +404,27 @@ def test_drawn_candidates_change_with_counter_and_seed():
     assert np.array_equal(a.argmax[other], b.argmax[other])  # greedy outside
 
 
+@pytest.mark.parametrize("M,d,V", [(2, 1 << 20, 257), (3, 64, 1000003)])
+def test_extreme_sizes(M, d, V):
+    """The largest supported hidden size (d = 2^20: 2 MiB rows, the limit of
+    the kernel's 32-bit tile offsets) and a vocabulary of about a million
+    entries (3907 vocabulary tiles), bf16, every row against the oracle."""
+    _need_gpu()
+    gen = torch.Generator().manual_seed(M + d + V)
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(torch.bfloat16)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(torch.bfloat16)
+    hb, Wb = host_bits(h), host_bits(W)
+    msk = np.ones(M, np.uint8)
+    tok = np.full(M, -1, np.int32)
+    bs = np.zeros(1, np.int32)
+    g = gpu_step(h.to(DEV), W.to(DEV), tok, msk, bs, 1, M, M, 0.5)
+    ref = oracle.row_stats(hb, Wb)
+    rep = Report()
+    compare_stats(g, ref, np.arange(M), hb, Wb, d, rep)
+    _say("extreme sizes M=%d d=%d V=%d: max err %s" % (
+        M, d, V, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+
+
 def test_caller_workspace_and_determinism():
     """Caller-provided workspace gives the same bits as the library one, and
     repeated runs are bit-identical (fixed merge order, no atomics)."""
