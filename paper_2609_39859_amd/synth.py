@@ -88,6 +88,10 @@ CONFIGS["tiny_peaked"] = CONFIGS["tiny"].with_(name="tiny_peaked",
                                                scale_args=(0.05, 3.0))
 CONFIGS["mid_planted"] = CONFIGS["mid"].with_(name="mid_planted", tau=0.5,
                                               plant_peaks=0.5)
+# The LLaDA-8B shape with planted peaks: 30% of the rows get one logit about
+# 20 above the rest (confidence near 1), so steps at d = 4096, V = 126464
+# commit several positions in parallel.
+CONFIGS["llada8b_planted"] = CONFIGS["llada8b"].with_(name="llada8b_planted", plant_peaks=0.3)
 # ForkGRPO rollouts in the paper's shape of a batch (groups of G = 16
 # rollouts per prompt, lambda = 0.8, blocks of 32), scaled down so that the
 # oracle follows a whole decode: 2 prompts x 16 rollouts, 64 generated

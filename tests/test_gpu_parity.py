@@ -569,6 +569,39 @@ def test_full_size_drawn_candidates(name, rows_mode):
         name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
 
 
+def test_full_size_planted_peaks_lockstep():
+    """Multi-commit parallel steps at the full LLaDA-8B shape (d = 4096,
+    V = 126464): three lock-step steps with planted peaks, every active row
+    against the oracle, decisions exact outside the exclusion sets."""
+    _need_gpu()
+    cfg = synth.CONFIGS["llada8b_planted"]
+    W = synth.weights(cfg, device=DEV)
+    Wb = host_bits(W)
+    tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+    B, L, BL = cfg.B, cfg.L, cfg.block_len
+    rep = Report()
+    multi = 0
+    for t in range(3):
+        h = synth.hidden(cfg, t, device=DEV, W=W)
+        hb = host_bits(h)
+        rows = _active_rows(cfg, msk, bs)
+        _say("planted full-size step %d: GPU step, oracle on %d rows" % (t, rows.size))
+        g = gpu_step(h, W, tok, msk, bs, B, L, BL, cfg.tau)
+        ref = oracle.row_stats(hb, Wb, rows)
+        ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
+        conf_full = np.full(cfg.M, np.nan)
+        am_full = np.zeros(cfg.M, np.int32)
+        conf_full[rows], am_full[rows] = ref["conf"], ref["argmax"]
+        sel = oracle.select(conf_full, am_full, tok, msk, bs, B, L, BL, _lam(cfg.tau))
+        compare_decisions(g, sel, conf_full, tok, msk, bs, B, L, BL, cfg.tau, rep,
+                          near_tie_rows=ties)
+        multi += int(np.sum(sel[4] > 1))
+        tok, msk, bs = sel[0], sel[1], sel[2]
+    assert multi >= 4, "expected parallel multi-commit steps, got %d" % multi
+    _say("planted full-size: %d rows (%d near-tie), %d multi-commit sequence-steps, max err %s" % (
+        rep.rows, rep.near_tie_rows, multi, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+
+
 @pytest.mark.parametrize("name", ["llada8b"])
 def test_full_size_decode_is_autoregressive(name):
     """A whole decode at the full LLaDA-8B shape on the GPU: with no

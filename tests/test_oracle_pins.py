@@ -654,3 +654,54 @@ def test_top_entropy_rejects_bad_k(orc):
         orc.top_entropy(np.zeros((2, 5)), 6)
     with pytest.raises(ValueError):
         orc.top_entropy(np.zeros((2, 5)), -1)
+
+
+# ------------------------------------------------ randomised selection properties
+
+from hypothesis import given, settings, strategies as st  # noqa: E402
+
+
+@settings(max_examples=200, deadline=None)
+@given(B=st.integers(1, 4), L=st.integers(1, 40), BL=st.integers(1, 40),
+       lam=st.sampled_from([0.0, 0.3, 0.9, 1.0]), rule=st.integers(0, 4),
+       seed=st.integers(0, 2 ** 31 - 1))
+def test_select_properties_hypothesis(B, L, BL, lam, rule, seed):
+    """One application of the rule on random states: commits lie in the
+    active block and were masked; a fallback step commits exactly one
+    position; otherwise every masked position above lambda in the block is
+    committed and nothing else; committed tokens are the candidates; idle
+    sequences are untouched."""
+    orc = oracle.default()
+    BL = min(BL, L)
+    rng = np.random.default_rng(seed)
+    M = B * L
+    conf = rng.random(M).astype(np.float32).astype(np.float64)
+    ent = rng.random(M)
+    am = rng.integers(0, 50, M).astype(np.int32)
+    msk = (rng.random(M) < 0.6).astype(np.uint8)
+    tok = np.where(msk, -1, 7).astype(np.int32)
+    bs = rng.integers(0, L + 1, B).astype(np.int32)
+    uni = rng.random(B).astype(np.float32)
+    t2, m2, b2, fb, nc = orc.select_ex(conf, am, tok, msk, bs, B, L, BL, lam, rule,
+                                       entropy=ent, uniform=uni)
+    for b in range(B):
+        sl = slice(b * L, (b + 1) * L)
+        committed = np.nonzero(msk[sl] & (1 - m2[sl]))[0]
+        assert np.all(m2[sl] <= msk[sl])                       # monotone mask
+        assert np.array_equal(t2[sl][committed], am[sl][committed])
+        untouched = np.setdiff1d(np.arange(L), committed)
+        assert np.array_equal(t2[sl][untouched], tok[sl][untouched])
+        masked = [k for k in range(int(bs[b]), L) if msk[b * L + k]]
+        if not masked:
+            assert fb[b] == -1 and committed.size == 0 and b2[b] == bs[b]
+            continue
+        s = int(b2[b])
+        assert (s - int(bs[b])) % BL == 0 and s <= masked[0] < s + BL
+        blk = [k for k in masked if k < s + BL]
+        passing = [k for k in blk if conf[b * L + k] > lam]
+        assert np.all((committed >= s) & (committed < s + BL))
+        if passing:
+            assert fb[b] == 0 and committed.tolist() == passing
+        else:
+            assert fb[b] == 1 and committed.size == 1 and committed[0] in blk
+        assert nc[b] == committed.size
