@@ -29,14 +29,16 @@ namespace fork {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kMergeRows = 64;    // positions per merge workgroup (one per lane)
-constexpr int kMergeWaves = 16;   // waves splitting the vocabulary tiles
+constexpr int kMergePositions = 16;  // positions per merge workgroup
+constexpr int kMergeWaves = 16;      // waves per workgroup, 4 tile streams each
+constexpr int kMergeThreads = 64 * kMergeWaves;
 
 __device__ __forceinline__ float4 merge2(float4 a, float4 b) {
   if (b.y == 0.f) return a;
   if (a.y == 0.f) return b;
   const float m = fmaxf(a.x, b.x);
-  const float ea = exp2f((a.x - m) * kLog2e), eb = exp2f((b.x - m) * kLog2e);
+  const float ea = __builtin_amdgcn_exp2f((a.x - m) * kLog2e);
+  const float eb = __builtin_amdgcn_exp2f((b.x - m) * kLog2e);
   float4 r;
   r.x = m;
   r.y = a.y * ea + b.y * eb;
@@ -54,56 +56,110 @@ __device__ __forceinline__ float4 pick_drawn(float4 a, float4 b) {
   return make_float4(take_a ? a.x : b.x, take_a ? a.y : b.y, take_a ? a.z : b.z, 0.f);
 }
 
-__global__ __launch_bounds__(kMergeRows * kMergeWaves) void merge_kernel(
+__device__ __forceinline__ float4 shfl_xor4(float4 v, int off) {
+  return make_float4(__shfl_xor(v.x, off), __shfl_xor(v.y, off), __shfl_xor(v.z, off),
+                     __shfl_xor(v.w, off));
+}
+
+// 16 positions per workgroup of 16 waves.  Lane l of wave w serves position
+// l % 16 and tile stream c = 4 w + l / 16 (64 streams): it merges tiles
+// c, c + 64, ... in increasing order, loads issued four at a time, so one
+// load instruction reads four runs of 16 consecutive positions (256 B each).
+// The 64 stream results of a position are then combined in a fixed tree —
+// lanes l, l ^ 16, l ^ 32 by shuffles, then the 16 waves through LDS (four
+// at a time, then pairwise) — each pair merged as (lower, higher).  The result depends only on
+// the tile order, not on M, the grid or the row list.
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     const float4* __restrict__ partials, int M, int nvt, float* __restrict__ conf,
     float* __restrict__ entropy, float* __restrict__ logp, float* __restrict__ lse,
     int32_t* __restrict__ argmax, const int32_t* __restrict__ rowlist,
     const int32_t* __restrict__ sample_row, const float4* __restrict__ spartials,
     const int32_t* __restrict__ token, const float* __restrict__ ztoken, int V) {
-  __shared__ float4 red[kMergeWaves][kMergeRows];
-  __shared__ float4 sred[kMergeWaves][kMergeRows];
+  __shared__ float4 red[kMergeWaves][kMergePositions];
+  __shared__ float4 sred[kMergeWaves][kMergePositions];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int r = blockIdx.x * kMergeRows + lane;
+  const int pl = lane & 15;                  // position within the workgroup
+  const int c = 4 * w + (lane >> 4);         // tile stream 0..63
+  const int r = blockIdx.x * kMergePositions + pl;
+  const bool live = r < M;
   float4 acc = make_float4(-INFINITY, 0.f, 0.f, __int_as_float(0x7fffffff));
-  if (r < M)
-    for (int j = w; j < nvt; j += kMergeWaves)
-      acc = merge2(acc, partials[(size_t)j * M + r]);
-  red[w][lane] = acc;
-  // drawn candidate (positions marked in sample_row)
-  const bool drawn = sample_row && r < M && sample_row[r] >= 0;
-  float4 sacc = make_float4(-INFINITY, __int_as_float(0x7fffffff), 0.f, 0.f);
-  if (drawn)
-    for (int j = w; j < nvt; j += kMergeWaves)
-      sacc = pick_drawn(sacc, spartials[(size_t)j * M + r]);
-  sred[w][lane] = sacc;
-  __syncthreads();
-  const int dst = r < M ? (rowlist ? rowlist[r] : r) : -1;
-  if (w == 0 && dst >= 0) {
-#pragma unroll
-    for (int k = 1; k < kMergeWaves; ++k) acc = merge2(acc, red[k][lane]);
-    const float log_s = logf(acc.y);
-    if (entropy) entropy[dst] = log_s - acc.z / acc.y;
-    if (lse) lse[dst] = acc.x + log_s;
-    if (argmax) argmax[dst] = __float_as_int(acc.w);
-    if (token) {
-      // teacher-forced: log q of the given token from its logit
-      const int tk = token[r];
-      const float lq = (tk >= 0 && tk < V) ? (ztoken[r] - acc.x) - log_s : __int_as_float(0x7fc00000);
-      logp[dst] = lq;
-      if (conf) conf[dst] = exp2f(lq * kLog2e);
-    } else if (drawn) {
-#pragma unroll
-      for (int k = 1; k < kMergeWaves; ++k) sacc = pick_drawn(sacc, sred[k][lane]);
-      // untempered q of the drawn token: exp(z - m) / s
-      const float dz = sacc.z - acc.x;
-      conf[dst] = exp2f(dz * kLog2e) / acc.y;
-      logp[dst] = dz - log_s;
-      argmax[dst] = __float_as_int(sacc.y);
-    } else {
-      if (conf) conf[dst] = 1.0f / acc.y;
-      logp[dst] = -log_s;
+  if (live) {
+    const float4* col = partials + r;
+    int j = c;
+    for (; j + 192 < nvt; j += 256) {
+      const float4 p0 = col[(size_t)j * M], p1 = col[(size_t)(j + 64) * M];
+      const float4 p2 = col[(size_t)(j + 128) * M], p3 = col[(size_t)(j + 192) * M];
+      acc = merge2(merge2(merge2(merge2(acc, p0), p1), p2), p3);
     }
+    for (; j < nvt; j += 64) acc = merge2(acc, col[(size_t)j * M]);
+  }
+  // streams 4w + {0..3} of this position: lanes pl, pl + 16, pl + 32, pl + 48
+#pragma unroll
+  for (int off = 16; off <= 32; off <<= 1) {
+    const float4 o = shfl_xor4(acc, off);
+    acc = (lane & off) ? merge2(o, acc) : merge2(acc, o);
+  }
+  if (lane < 16) red[w][pl] = acc;
+  const bool drawn = sample_row && live && sample_row[r] >= 0;
+  float4 sacc = make_float4(-INFINITY, __int_as_float(0x7fffffff), 0.f, 0.f);
+  if (drawn) {
+    const float4* scol = spartials + r;
+    for (int k = c; k < nvt; k += 64) sacc = pick_drawn(sacc, scol[(size_t)k * M]);
+  }
+  if (sample_row) {
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float4 o = shfl_xor4(sacc, off);
+      sacc = (lane & off) ? pick_drawn(o, sacc) : pick_drawn(sacc, o);
+    }
+    if (lane < 16) sred[w][pl] = sacc;
+  }
+  __syncthreads();
+  if (w != 0) return;
+  // wave 0 combines the 16 wave results: lane group q = lane / 16 merges
+  // waves 4q .. 4q + 3, then the four groups pairwise
+  const int q = lane >> 4;
+  acc = red[4 * q][pl];
+#pragma unroll
+  for (int k = 1; k < 4; ++k) acc = merge2(acc, red[4 * q + k][pl]);
+#pragma unroll
+  for (int off = 16; off <= 32; off <<= 1) {
+    const float4 o = shfl_xor4(acc, off);
+    acc = (lane & off) ? merge2(o, acc) : merge2(acc, o);
+  }
+  if (sample_row) {
+    sacc = sred[4 * q][pl];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) sacc = pick_drawn(sacc, sred[4 * q + k][pl]);
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float4 o = shfl_xor4(sacc, off);
+      sacc = (lane & off) ? pick_drawn(o, sacc) : pick_drawn(sacc, o);
+    }
+  }
+  if (lane >= 16 || !live) return;
+  const int dst = rowlist ? rowlist[r] : r;
+  if (dst < 0) return;
+  const float log_s = logf(acc.y);
+  if (entropy) entropy[dst] = log_s - acc.z / acc.y;
+  if (lse) lse[dst] = acc.x + log_s;
+  if (argmax) argmax[dst] = __float_as_int(acc.w);
+  if (token) {
+    // teacher-forced: log q of the given token from its logit
+    const int tk = token[r];
+    const float lq = (tk >= 0 && tk < V) ? (ztoken[r] - acc.x) - log_s : __int_as_float(0x7fc00000);
+    logp[dst] = lq;
+    if (conf) conf[dst] = exp2f(lq * kLog2e);
+  } else if (drawn) {
+    // untempered q of the drawn token: exp(z - m) / s
+    const float dz = sacc.z - acc.x;
+    conf[dst] = exp2f(dz * kLog2e) / acc.y;
+    logp[dst] = dz - log_s;
+    argmax[dst] = __float_as_int(sacc.y);
+  } else {
+    if (conf) conf[dst] = 1.0f / acc.y;
+    logp[dst] = -log_s;
   }
 }
 
@@ -465,8 +521,8 @@ hipError_t launch_merge(const float4* partials, int M, int nvt, float* conf,
                         const int32_t* rowlist, const int32_t* sample_row,
                         const float4* spartials, const int32_t* token, const float* ztoken,
                         int V, hipStream_t stream) {
-  const dim3 grid((unsigned)((M + kMergeRows - 1) / kMergeRows));
-  const dim3 block(kMergeRows * kMergeWaves);
+  const dim3 grid((unsigned)((M + kMergePositions - 1) / kMergePositions));
+  const dim3 block(kMergeThreads);
   hipLaunchKernelGGL(merge_kernel, grid, block, 0, stream, partials, M, nvt, conf,
                      entropy, logp, lse, argmax, rowlist, sample_row, spartials, token, ztoken,
                      V);
