@@ -33,9 +33,11 @@
  *     and return a negative status; fork_last_error() then describes them.
  *   - Output arrays must not alias inputs.  tokens, mask and block_start are
  *     updated in place.
- *   - Concurrent calls that use the library-managed workspace must be issued
- *     on one stream (or serialised by the caller); callers that overlap
- *     calls on several streams pass their own workspace to fork_step_ex.
+ *   - Calls may come from several host threads.  Calls that use the
+ *     library-managed workspace of a device share one buffer, so their GPU
+ *     work must not overlap: issue them on one stream (or order the streams).
+ *     Callers that overlap calls on several streams pass their own workspace
+ *     to fork_step_ex / fork_logprob.
  */
 #ifndef FORK_STEP_H
 #define FORK_STEP_H

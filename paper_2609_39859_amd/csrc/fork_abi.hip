@@ -64,11 +64,16 @@ struct DeviceWorkspace {
 std::mutex g_ws_mutex;
 std::vector<DeviceWorkspace> g_ws;  // indexed by device ordinal
 
-int get_workspace(size_t need, void** out) {
+// Returns the current device's library-managed buffer (grown to `need`
+// bytes) with *lock holding g_ws_mutex.  The caller keeps the lock until its
+// kernels are enqueued, so another thread can neither free the buffer (to grow
+// it, or in fork_release) between this call and those launches; a later free
+// synchronises the device first, so enqueued work finishes before it.
+int get_workspace(size_t need, void** out, std::unique_lock<std::mutex>* lock) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(FORK_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
-  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  *lock = std::unique_lock<std::mutex>(g_ws_mutex);
   if ((int)g_ws.size() <= dev) g_ws.resize(dev + 1);
   DeviceWorkspace& ws = g_ws[dev];
   if (ws.bytes < need) {
@@ -156,12 +161,13 @@ int fork_step_ex(const fork_step_args* a) {
   Layout lay;
   if (!layout_for(a->B, a->L, a->V, sampling, &lay)) return fail(FORK_EINVAL, "invalid sizes");
   void* ws = a->workspace;
+  std::unique_lock<std::mutex> ws_lock;  // held until the launches are enqueued
   if (ws) {
     if (a->workspace_bytes < lay.total)
       return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, lay.total);
     if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
   } else {
-    rc = get_workspace(lay.total, &ws);
+    rc = get_workspace(lay.total, &ws, &ws_lock);
     if (rc != FORK_OK) return rc;
   }
   const int Mh = a->B * a->L;                       // rows of hidden
@@ -292,12 +298,13 @@ int fork_logprob(const fork_logprob_args* a) {
   if (!logprob_layout(a->n, a->V, &zt_off, &total)) return fail(FORK_EINVAL, "invalid sizes");
   if (a->n == 0) return FORK_OK;
   void* ws = a->workspace;
+  std::unique_lock<std::mutex> ws_lock;  // held until the launches are enqueued
   if (ws) {
     if (a->workspace_bytes < total)
       return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, total);
     if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
   } else {
-    int rc = get_workspace(total, &ws);
+    int rc = get_workspace(total, &ws, &ws_lock);
     if (rc != FORK_OK) return rc;
   }
   float4* partials = static_cast<float4*>(ws);
