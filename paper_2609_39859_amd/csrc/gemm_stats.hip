@@ -61,6 +61,7 @@ constexpr int kOperandBytes = 256 * kSlab;   // 32 KiB: one operand, one stage
 constexpr int kGroupV = 8;                   // vocab stripes per sweep group
 constexpr int kXcds = 8;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 // Raw-buffer descriptor word 3 for gfx9-family buffers: 32-bit data format,
 // offsets checked against the record count (out of range reads return 0).
 constexpr int kBufferWord3 = 0x00020000;
@@ -129,7 +130,6 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
 // avoids the cancellation of a logarithm near 1.  The key carries a relative
 // error of about 1e-6 in E, far below the logit rounding.
 __device__ __forceinline__ float gumbel_key(float z, float inv_tau, uint32_t w) {
-  constexpr float kLn2 = 0.6931471805599453f;
   const float u = (float)(2u * (w >> 9) + 1u) * 0x1p-24f;
   const float series = u * fmaf(u, fmaf(u, fmaf(u, 0.25f, 1.0f / 3.0f), 0.5f), 1.0f);
   const float viaLog = -__builtin_amdgcn_logf(1.0f - u) * kLn2;
@@ -152,57 +152,82 @@ enum EpilogueMode { kGreedy = 0, kDrawn = 1, kTarget = 2 };
 // Drawn candidates (kDrawn) go through a second LDS exchange and a second
 // partials array (see SampleArgs); the logit of a given token (kTarget) is
 // stored by the one lane that holds it.
-template <int kMode>
-__device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned char* smem, int tid,
-                                         int lane, int wv, int wp, int vt, int v0, int p0, int M,
-                                         int V, float4* __restrict__ partials,
-                                         const SampleArgs& sa, const TargetArgs& ta) {
-  constexpr bool kDraw = kMode == kDrawn;
-  float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
-  float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
-  const int vbase = v0 + wv * 128;
-  const bool full = v0 + kTileV <= V;
+// Statistics of the 64 logits one lane holds for column j (rows vbase +
+// acc_row(i, e, lane), increasing in (i, e)), combined with the lane 32
+// apart that holds the other 64 rows of the column: the maximum m, the
+// lowest row holding it, s = sum e^(z-m) and t = sum e^(z-m)(z-m).
+// Branch-free.  Unless kFull (every row < V), rows past V are set to -inf in
+// acc first, so that no pass needs a row test.
+template <bool kFull>
+__device__ __forceinline__ void column_stats(f32x16 (&acc)[4][2], int j, int lane, int vbase,
+                                             int V, float& m_out, int& idx_out, float& s_out,
+                                             float& t_out) {
+  if (!kFull) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    // maximum and its lowest index; values are visited in increasing v
-    float m = -INFINITY;
-    int idx = 0x7fffffff;
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (vbase + acc_row(i, e, lane) >= V) acc[i][j][e] = -INFINITY;
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) m = fmaxf(m, acc[i][j][e]);
+  // the lowest row holding m: scan from the highest row down
+  int idx = 0x7fffffff;
+#pragma unroll
+  for (int i = 3; i >= 0; --i)
+#pragma unroll
+    for (int e = 15; e >= 0; --e) idx = acc[i][j][e] == m ? vbase + acc_row(i, e, lane) : idx;
+  {
+    const float mo = __shfl_xor(m, 32);
+    const int io = __shfl_xor(idx, 32);
+    const bool take = mo > m || (mo == m && io < idx);
+    m = take ? mo : m;
+    idx = take ? io : idx;
+  }
+  float s = 0.f, tl = 0.f;
+  if (m > -INFINITY) {
+    const float nml = -m * kLog2e;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int v = vbase + acc_row(i, e, lane);
-        const float z = acc[i][j][e];
-        if ((full || v < V) && z > m) {
-          m = z;
-          idx = v;
-        }
+        // (z - m) * log2(e) with one rounding; the moment is summed in
+        // these units and scaled by ln 2 once
+        const float dl = fmaf(acc[i][j][e], kLog2e, nml);
+        const float ex = __builtin_amdgcn_exp2f(dl);
+        s += ex;
+        // a -inf row has ex = 0: keep 0 * -inf out of the moment
+        tl = fmaf(ex, kFull ? dl : fmaxf(dl, -1e30f), tl);
       }
-    {
-      const float mo = __shfl_xor(m, 32);
-      const int io = __shfl_xor(idx, 32);
-      if (mo > m || (mo == m && io < idx)) {
-        m = mo;
-        idx = io;
-      }
-    }
-    float s = 0.f, t = 0.f;
-    if (m > -INFINITY) {
+  }
+  s += __shfl_xor(s, 32);
+  tl += __shfl_xor(tl, 32);
+  m_out = m;
+  idx_out = idx;
+  s_out = s;
+  t_out = tl * kLn2;
+}
+
+// kFull: the tile's 256 vocabulary rows are all < V (every tile but a
+// ragged last one), so no row test is compiled in.
+template <int kMode, bool kFull>
+__device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char* smem, int tid,
+                                              int lane, int wv, int wp, int vt, int v0, int p0,
+                                              int M, int V, float4* __restrict__ partials,
+                                              const SampleArgs& sa, const TargetArgs& ta) {
+  constexpr bool kDraw = kMode == kDrawn;
+  constexpr bool full = kFull;
+  float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
+  float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
+  const int vbase = v0 + wv * 128;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int v = vbase + acc_row(i, e, lane);
-          if (full || v < V) {
-            const float dz = acc[i][j][e] - m;
-            const float ex = __builtin_amdgcn_exp2f(dz * kLog2e);
-            s += ex;
-            t = fmaf(ex, dz, t);
-          }
-        }
-    }
-    s += __shfl_xor(s, 32);
-    t += __shfl_xor(t, 32);
+  for (int j = 0; j < 2; ++j) {
+    float m, s, t;
+    int idx;
+    column_stats<kFull>(acc, j, lane, vbase, V, m, idx, s, t);
     const int col = wp * 64 + j * 32 + (lane & 31);
     if (lane < 32) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
     if (kMode == kTarget) {
@@ -274,6 +299,17 @@ __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], unsigned cha
       }
     }
   }
+}
+
+template <int kMode>
+__device__ __forceinline__ void epilogue(f32x16 (&acc)[4][2], unsigned char* smem, int tid,
+                                         int lane, int wv, int wp, int vt, int v0, int p0, int M,
+                                         int V, float4* __restrict__ partials,
+                                         const SampleArgs& sa, const TargetArgs& ta) {
+  if (v0 + kTileV <= V)
+    epilogue_tile<kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+  else
+    epilogue_tile<kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
 }
 
 __device__ __forceinline__ void barrier_nofence() {
