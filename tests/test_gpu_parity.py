@@ -158,6 +158,60 @@ def test_crafted_ties_and_layout():
         assert np.all(g.fallback == -1) and np.all(g.ncommit == 0)
 
 
+def test_crafted_ragged_tile_boundary():
+    """V = 300: the second vocabulary tile holds 44 rows.  One-hot hidden
+    rows select one column of W, so the logits of a position are that column
+    exactly.  Columns: the maximum at the last row (299), at the first row of
+    the ragged tile (256), tied across the tile boundary (255 and 256: the
+    lower wins), all logits far below zero, a ragged tile far below the
+    maximum, and all logits equal.  Checks candidate, confidence, entropy
+    and log-probability against closed forms and the oracle, and the
+    teacher-forced log-probability of tokens on both sides of the boundary."""
+    _need_gpu()
+    V, d = 300, 8
+    cols = np.full((V, 6), -1.0, np.float32)
+    cols[299, 0] = 1.0
+    cols[256, 1] = 1.0
+    cols[255, 2] = cols[256, 2] = 1.0
+    cols[:, 3] = -50.0
+    cols[280, 3] = -40.0
+    cols[:256, 4] = 0.0
+    cols[256:, 4] = -30.0
+    cols[7, 4] = 2.0
+    cols[:, 5] = 0.5
+    want = np.array([299, 256, 255, 280, 7, 0])
+    for dtype in (torch.float32, torch.bfloat16):
+        B, L = 1, 12
+        M = B * L
+        hot = np.arange(M) % 6
+        h = torch.zeros(M, d)
+        h[torch.arange(M), torch.as_tensor(hot)] = 1.0
+        W = torch.zeros(V, d)
+        W[:, :6] = torch.as_tensor(cols)
+        h, W = h.to(dtype), W.to(dtype)
+        g = gpu_step(h.to(DEV), W.to(DEV), np.zeros(M, np.int32), np.zeros(M, np.uint8),
+                     np.zeros(B, np.int32), B, L, L, 0.5)
+        assert np.array_equal(g.argmax, want[hot])
+        z = cols[:, hot].T.astype(np.float64)                 # [M, V] exact logits
+        zm = z.max(axis=1, keepdims=True)
+        p = np.exp(z - zm) / np.exp(z - zm).sum(axis=1, keepdims=True)
+        np.testing.assert_allclose(g.conf, p.max(axis=1), atol=2e-6, rtol=1e-5)
+        ent = -(p * np.log(np.where(p > 0, p, 1.0))).sum(axis=1)
+        np.testing.assert_allclose(g.entropy, ent, atol=2e-5)
+        lse = zm[:, 0] + np.log(np.exp(z - zm).sum(axis=1))
+        np.testing.assert_allclose(g.lse, lse, atol=2e-5, rtol=1e-6)
+        np.testing.assert_allclose(g.logp, z.max(axis=1) - lse, atol=2e-5)
+        ref = oracle.row_stats(host_bits(h), host_bits(W))
+        np.testing.assert_allclose(g.entropy, ref["entropy"], atol=2e-5)
+        np.testing.assert_allclose(g.logp, ref["logp"], atol=2e-5)
+        # teacher-forced tokens on both sides of the tile boundary
+        tgt = np.array([255, 256, 299, 0, 298, 257, 255, 256, 299, 0, 1, 280], np.int32)
+        out = torch.empty(M, dtype=torch.float32, device=DEV)
+        _binding.logprob(h.to(DEV), W.to(DEV), torch.as_tensor(tgt).to(DEV), out)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(out.cpu().numpy(), z[np.arange(M), tgt] - lse, atol=2e-5)
+
+
 @pytest.mark.parametrize("name", ["tiny", "tiny_peaked"])
 def test_tiny_lockstep_decode(name):
     _need_gpu()
