@@ -116,8 +116,11 @@ enum {
  * out_entropy  [B*L] float: entropy of q in nats for every position.
  * out_logp     [B*L] float: log q(candidate) for every position.
  * out_fallback [B] int32: FORK_STEP_* per sequence.
- * B, L, d, V   sizes, all >= 1, B*L < 2^31; d % 8 == 0 for FORK_BF16,
- *              d % 4 == 0 for FORK_F32, d <= 2^20 (else FORK_EUNSUPPORTED).
+ * B, L, d, V   sizes: L, d, V >= 1, B >= 0, B*L < 2^31; d % 8 == 0 for
+ *              FORK_BF16, d % 4 == 0 for FORK_F32, d <= 2^20 (else
+ *              FORK_EUNSUPPORTED).  B == 0 (an empty batch) enqueues
+ *              nothing and returns FORK_OK; the array pointers may then be
+ *              NULL.
  * dtype        FORK_BF16 or FORK_F32.
  * stream       hipStream_t to enqueue on (NULL = default stream).
  *
@@ -201,7 +204,8 @@ size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
    of fork_step_ex, with the same arguments, semantics and outputs
    (out_fallback per sequence; out_ncommit and out_commit_pos optional).
    entropy ([B*L]) is needed by FORK_RULE_MAXENT, uniform ([B]) by
-   FORK_RULE_RANDOM.  Returns FORK_OK, FORK_EINVAL or FORK_EHIP. */
+   FORK_RULE_RANDOM.  B == 0 enqueues nothing (array pointers may be NULL).
+   Returns FORK_OK, FORK_EINVAL or FORK_EHIP. */
 typedef struct fork_select_args {
   const float* conf;       /* [B*L] confidence of each position's candidate    */
   const float* entropy;    /* [B*L] or NULL                                    */

@@ -110,11 +110,12 @@ bool grid_fits(long long positions, int V) {
 
 int validate(const fork_step_args* a) {
   if (!a) return fail(FORK_EINVAL, "args is NULL");
-  if (!a->hidden || !a->W_head || !a->tokens || !a->mask || !a->block_start || !a->out_conf ||
-      !a->out_entropy || !a->out_logp || !a->out_fallback)
+  if (a->B < 0 || a->L <= 0 || a->d <= 0 || a->V <= 0)
+    return fail(FORK_EINVAL, "need B >= 0 and L, d, V > 0 (B=%d L=%d d=%d V=%d)", a->B, a->L,
+                a->d, a->V);
+  if (a->B > 0 && (!a->hidden || !a->W_head || !a->tokens || !a->mask || !a->block_start ||
+                   !a->out_conf || !a->out_entropy || !a->out_logp || !a->out_fallback))
     return fail(FORK_EINVAL, "a required pointer is NULL");
-  if (a->B <= 0 || a->L <= 0 || a->d <= 0 || a->V <= 0)
-    return fail(FORK_EINVAL, "sizes must be positive (B=%d L=%d d=%d V=%d)", a->B, a->L, a->d, a->V);
   if ((long long)a->B * a->L > 0x7fffffffLL)
     return fail(FORK_EINVAL, "B*L = %lld does not fit int32", (long long)a->B * a->L);
   if (a->block_len <= 0 || a->block_len > a->L)
@@ -124,7 +125,7 @@ int validate(const fork_step_args* a) {
     return fail(FORK_EINVAL, "unknown dtype %d", a->dtype);
   if (a->rule < FORK_RULE_LEFTMOST || a->rule > FORK_RULE_RANDOM)
     return fail(FORK_EINVAL, "unknown fallback rule %d", a->rule);
-  if (a->rule == FORK_RULE_RANDOM && !a->fallback_uniform)
+  if (a->rule == FORK_RULE_RANDOM && a->B > 0 && !a->fallback_uniform)
     return fail(FORK_EINVAL, "FORK_RULE_RANDOM needs fallback_uniform");
   if (a->dtype == FORK_BF16 && a->d % 8 != 0)
     return fail(FORK_EUNSUPPORTED, "bf16 path needs d %% 8 == 0 (d=%d)", a->d);
@@ -157,6 +158,7 @@ extern "C" {
 int fork_step_ex(const fork_step_args* a) {
   int rc = validate(a);
   if (rc != FORK_OK) return rc;
+  if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
   const bool sampling = a->sample_temperature > 0.0f;
   Layout lay;
   if (!layout_for(a->B, a->L, a->V, sampling, &lay)) return fail(FORK_EINVAL, "invalid sizes");
@@ -332,9 +334,10 @@ int fork_logprob(const fork_logprob_args* a) {
 
 int fork_select(const fork_select_args* a) {
   if (!a) return fail(FORK_EINVAL, "args is NULL");
-  if (!a->conf || !a->argmax || !a->tokens || !a->mask || !a->block_start || !a->out_fallback)
+  if (a->B < 0 || a->L <= 0) return fail(FORK_EINVAL, "need B >= 0 and L > 0 (B=%d L=%d)", a->B, a->L);
+  if (a->B > 0 && (!a->conf || !a->argmax || !a->tokens || !a->mask || !a->block_start ||
+                   !a->out_fallback))
     return fail(FORK_EINVAL, "a required pointer is NULL");
-  if (a->B <= 0 || a->L <= 0) return fail(FORK_EINVAL, "sizes must be positive (B=%d L=%d)", a->B, a->L);
   if ((long long)a->B * a->L > 0x7fffffffLL)
     return fail(FORK_EINVAL, "B*L = %lld does not fit int32", (long long)a->B * a->L);
   if (a->block_len <= 0 || a->block_len > a->L)
@@ -342,10 +345,11 @@ int fork_select(const fork_select_args* a) {
   if (!isfinite(a->tau)) return fail(FORK_EINVAL, "tau must be finite");
   if (a->rule < FORK_RULE_LEFTMOST || a->rule > FORK_RULE_RANDOM)
     return fail(FORK_EINVAL, "unknown fallback rule %d", a->rule);
-  if (a->rule == FORK_RULE_RANDOM && !a->uniform)
+  if (a->rule == FORK_RULE_RANDOM && a->B > 0 && !a->uniform)
     return fail(FORK_EINVAL, "FORK_RULE_RANDOM needs uniform");
-  if (a->rule == FORK_RULE_MAXENT && !a->entropy)
+  if (a->rule == FORK_RULE_MAXENT && a->B > 0 && !a->entropy)
     return fail(FORK_EINVAL, "FORK_RULE_MAXENT needs entropy");
+  if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
   hipError_t e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->conf,
                                      a->entropy, a->uniform, a->argmax, a->tokens, a->mask,
                                      a->block_start, a->out_fallback, a->out_ncommit,

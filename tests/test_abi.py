@@ -70,7 +70,7 @@ def _args(**kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(hidden=0), _binding.FORK_EINVAL),
     (dict(out_fallback=0), _binding.FORK_EINVAL),
-    (dict(B=0), _binding.FORK_EINVAL),
+    (dict(B=-1), _binding.FORK_EINVAL),
     (dict(V=-3), _binding.FORK_EINVAL),
     (dict(block_len=0), _binding.FORK_EINVAL),
     (dict(block_len=9), _binding.FORK_EINVAL),
@@ -102,6 +102,24 @@ def test_bad_arguments_rejected_on_host(kw, code):
     a = _args(**kw)
     assert L.fork_step_ex(ctypes.byref(a)) == code
     assert L.fork_last_error().decode() != ""
+
+
+def test_empty_batch_is_a_no_op():
+    """B == 0 returns before any HIP call, with every array pointer NULL; the
+    scalar arguments are still checked."""
+    L = _binding.lib()
+    nulls = dict(hidden=0, W_head=0, tokens=0, mask=0, block_start=0, out_conf=0,
+                 out_entropy=0, out_logp=0, out_fallback=0, B=0)
+    assert L.fork_step_ex(ctypes.byref(_args(**nulls))) == _binding.FORK_OK
+    assert L.fork_step_ex(ctypes.byref(_args(rule=4, **nulls))) == _binding.FORK_OK
+    assert L.fork_step_ex(ctypes.byref(_args(tau=float("nan"), **nulls))) == _binding.FORK_EINVAL
+    assert L.fork_step_ex(ctypes.byref(_args(block_len=9, **nulls))) == _binding.FORK_EINVAL
+    assert L.fork_step(None, None, None, None, None, 4, 0.9, None, None, None, None,
+                       0, 8, 16, 100, _binding.FORK_BF16, None) == _binding.FORK_OK
+    sel_nulls = dict(conf=0, argmax=0, tokens=0, mask=0, block_start=0, out_fallback=0, B=0)
+    assert L.fork_select(ctypes.byref(_sel_args(**sel_nulls))) == _binding.FORK_OK
+    assert L.fork_select(ctypes.byref(_sel_args(rule=3, **sel_nulls))) == _binding.FORK_OK
+    assert L.fork_select(ctypes.byref(_sel_args(rule=7, **sel_nulls))) == _binding.FORK_EINVAL
 
 
 def test_null_args_struct():
@@ -215,7 +233,7 @@ def _sel_args(**kw):
 
 @pytest.mark.parametrize("kw", [
     dict(conf=0), dict(argmax=0), dict(tokens=0), dict(mask=0), dict(block_start=0),
-    dict(out_fallback=0), dict(B=0), dict(L=-1), dict(block_len=0), dict(block_len=9),
+    dict(out_fallback=0), dict(B=-1), dict(L=-1), dict(block_len=0), dict(block_len=9),
     dict(tau=float("nan")), dict(rule=5), dict(rule=4), dict(rule=3),
     dict(B=1 << 16, L=1 << 16),
 ])
