@@ -33,11 +33,19 @@
  *     and return a negative status; fork_last_error() then describes them.
  *   - Output arrays must not alias inputs.  tokens, mask and block_start are
  *     updated in place.
- *   - Calls may come from several host threads.  Calls that use the
- *     library-managed workspace of a device share one buffer, so their GPU
- *     work must not overlap: issue them on one stream (or order the streams).
- *     Callers that overlap calls on several streams pass their own workspace
- *     to fork_step_ex / fork_logprob.
+ *   - Calls may come from several host threads and on several streams.
+ *     Calls that pass no workspace of their own use the library-managed
+ *     workspace of the (device, stream) pair they are enqueued on: calls on
+ *     one stream share a buffer (their work runs in stream order), calls on
+ *     different streams get different buffers and may overlap.  A buffer
+ *     that must grow is replaced by a larger one without synchronising; the
+ *     outgrown allocation is kept until fork_release, since work already
+ *     queued may still read it.  Each stream that has used the managed
+ *     workspace keeps its buffer until fork_release.
+ *   - Graph capture: a call that would use the managed workspace returns
+ *     FORK_EINVAL while its stream is being captured (the graph would keep
+ *     the buffer's address beyond fork_release).  Captured calls pass a
+ *     caller workspace, which must outlive the graph.
  */
 #ifndef FORK_STEP_H
 #define FORK_STEP_H
@@ -127,8 +135,9 @@ enum {
  * Returns FORK_OK or a negative FORK_E* code (FORK_EUNSUPPORTED also when
  * the launch grid would exceed 2^32 work-items, i.e. when
  * ceil(positions/256) * ceil(V/256) * 512 >= 2^32; split such batches).
- * Uses the library-managed workspace of the current device (grown on demand
- * with hipMalloc, which may synchronise the device; fork_release frees it).
+ * Uses the library-managed workspace of (device of `stream`, `stream`),
+ * grown on demand with hipMalloc; fork_release frees it.  Returns FORK_EINVAL
+ * while `stream` is being captured into a graph.
  */
 int fork_step(const void* hidden, const void* W_head, int32_t* tokens,
               uint8_t* mask, int32_t* block_start, int32_t block_len,
@@ -312,8 +321,10 @@ int fork_top_entropy(const float* entropy, int32_t R, int32_t Lg, int32_t k, uin
    The string stays valid until the thread's next call into the library. */
 const char* fork_last_error(void);
 
-/* Free the library-managed workspaces of every device.  Must not race with
-   work still using them (synchronise first). */
+/* Free the library-managed workspaces of every device and stream, outgrown
+   allocations included.  Synchronises each device that holds one first, so
+   work already queued finishes; must not race with calls still being
+   issued by other threads. */
 void fork_release(void);
 
 /* Library version as major*10000 + minor*100 + patch. */

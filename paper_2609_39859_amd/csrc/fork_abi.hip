@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "fork_kernels.h"
+#include "workspace_registry.h"
 
 namespace {
 
@@ -56,42 +57,61 @@ bool layout_for(int32_t B, int32_t L, int32_t V, bool sampling, Layout* out) {
   return true;
 }
 
-struct DeviceWorkspace {
-  void* ptr = nullptr;
-  size_t bytes = 0;
+// hipMalloc / hipFree / hipDeviceSynchronize on a given device, restoring
+// the caller's current device.
+struct HipBackend {
+  static int alloc(int dev, size_t bytes, void** out) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return FORK_EHIP;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return FORK_EHIP;
+    const hipError_t e = hipMalloc(out, bytes);
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !*out) {
+      fail(FORK_ENOMEM, "hipMalloc(%zu) for the workspace: %s", bytes, hipGetErrorString(e));
+      return FORK_ENOMEM;
+    }
+    return 0;
+  }
+  static void free(int dev, void* p) {
+    int cur = 0;
+    const bool have = hipGetDevice(&cur) == hipSuccess;
+    if (hipSetDevice(dev) == hipSuccess) (void)hipFree(p);
+    if (have) (void)hipSetDevice(cur);
+  }
+  static void sync(int dev) {
+    int cur = 0;
+    const bool have = hipGetDevice(&cur) == hipSuccess;
+    if (hipSetDevice(dev) == hipSuccess) (void)hipDeviceSynchronize();
+    if (have) (void)hipSetDevice(cur);
+  }
 };
 
-std::mutex g_ws_mutex;
-std::vector<DeviceWorkspace> g_ws;  // indexed by device ordinal
+fork::WorkspaceRegistry<HipBackend> g_registry;
 
-// Returns the current device's library-managed buffer (grown to `need`
-// bytes) with *lock holding g_ws_mutex.  The caller keeps the lock until its
-// kernels are enqueued, so another thread can neither free the buffer (to grow
-// it, or in fork_release) between this call and those launches; a later free
-// synchronises the device first, so enqueued work finishes before it.
-int get_workspace(size_t need, void** out, std::unique_lock<std::mutex>* lock) {
+// The device a stream belongs to (the current device for the NULL stream).
+int stream_device(hipStream_t stream, int* dev) {
+  hipError_t e = stream ? hipStreamGetDevice(stream, dev) : hipGetDevice(dev);
+  if (e != hipSuccess) return fail(FORK_EHIP, "device of the stream: %s", hipGetErrorString(e));
+  return FORK_OK;
+}
+
+// The library-managed buffer of (device of `stream`, `stream`), grown to
+// `need` bytes, with *lock holding the registry until the caller's launches
+// are enqueued.  Refused while the stream is being captured into a graph: a
+// graph would keep the buffer's address past fork_release.
+int get_workspace(hipStream_t stream, size_t need, void** out, std::unique_lock<std::mutex>* lock) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return fail(FORK_EHIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(FORK_EINVAL,
+                "the stream is being captured into a graph: pass a caller workspace "
+                "(workspace / workspace_bytes) that outlives the graph");
   int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(FORK_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
-  *lock = std::unique_lock<std::mutex>(g_ws_mutex);
-  if ((int)g_ws.size() <= dev) g_ws.resize(dev + 1);
-  DeviceWorkspace& ws = g_ws[dev];
-  if (ws.bytes < need) {
-    if (ws.ptr) {
-      // hipFree waits for work still using the old buffer
-      e = hipFree(ws.ptr);
-      ws.ptr = nullptr;
-      ws.bytes = 0;
-      if (e != hipSuccess) return fail(FORK_EHIP, "hipFree: %s", hipGetErrorString(e));
-    }
-    void* p = nullptr;
-    e = hipMalloc(&p, need);
-    if (e != hipSuccess || !p)
-      return fail(FORK_ENOMEM, "hipMalloc(%zu) for the workspace: %s", need, hipGetErrorString(e));
-    ws.ptr = p;
-    ws.bytes = need;
-  }
-  *out = ws.ptr;
+  int rc = stream_device(stream, &dev);
+  if (rc != FORK_OK) return rc;
+  rc = g_registry.acquire(dev, reinterpret_cast<uintptr_t>(stream), need, out, lock);
+  if (rc != 0) return rc == FORK_ENOMEM ? FORK_ENOMEM : fail(FORK_EHIP, "workspace allocation failed");
   return FORK_OK;
 }
 
@@ -151,27 +171,10 @@ int validate(const fork_step_args* a) {
   return FORK_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-int fork_step_ex(const fork_step_args* a) {
-  int rc = validate(a);
-  if (rc != FORK_OK) return rc;
-  if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
+// The launches of one step (active rows, LM head, merge, selection) on
+// the workspace `ws` laid out as `lay`; arguments already validated.
+int enqueue_step(const fork_step_args* a, void* ws, const Layout& lay) {
   const bool sampling = a->sample_temperature > 0.0f;
-  Layout lay;
-  if (!layout_for(a->B, a->L, a->V, sampling, &lay)) return fail(FORK_EINVAL, "invalid sizes");
-  void* ws = a->workspace;
-  std::unique_lock<std::mutex> ws_lock;  // held until the launches are enqueued
-  if (ws) {
-    if (a->workspace_bytes < lay.total)
-      return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, lay.total);
-    if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
-  } else {
-    rc = get_workspace(lay.total, &ws, &ws_lock);
-    if (rc != FORK_OK) return rc;
-  }
   const int Mh = a->B * a->L;                       // rows of hidden
   const bool active = a->rows_mode == FORK_ROWS_ACTIVE;
   const int M = active ? a->B * a->block_len : Mh;  // positions through the LM head
@@ -230,6 +233,30 @@ int fork_step_ex(const fork_step_args* a) {
     if (e != hipSuccess) return fail(FORK_EHIP, "step failed: %s", hipGetErrorString(e));
   }
   return FORK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fork_step_ex(const fork_step_args* a) {
+  int rc = validate(a);
+  if (rc != FORK_OK) return rc;
+  if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
+  const bool sampling = a->sample_temperature > 0.0f;
+  Layout lay;
+  if (!layout_for(a->B, a->L, a->V, sampling, &lay)) return fail(FORK_EINVAL, "invalid sizes");
+  void* ws = a->workspace;
+  std::unique_lock<std::mutex> ws_lock;  // held until the launches are enqueued
+  if (ws) {
+    if (a->workspace_bytes < lay.total)
+      return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, lay.total);
+    if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
+  } else {
+    rc = get_workspace(static_cast<hipStream_t>(a->stream), lay.total, &ws, &ws_lock);
+    if (rc != FORK_OK) return rc;
+  }
+  return enqueue_step(a, ws, lay);
 }
 
 int fork_step(const void* hidden, const void* W_head, int32_t* tokens, uint8_t* mask,
@@ -306,7 +333,7 @@ int fork_logprob(const fork_logprob_args* a) {
       return fail(FORK_EINVAL, "workspace holds %zu bytes, %zu needed", a->workspace_bytes, total);
     if (((uintptr_t)ws % kAlign) != 0) return fail(FORK_EINVAL, "workspace must be 256-byte aligned");
   } else {
-    int rc = get_workspace(total, &ws, &ws_lock);
+    int rc = get_workspace(static_cast<hipStream_t>(a->stream), total, &ws, &ws_lock);
     if (rc != FORK_OK) return rc;
   }
   float4* partials = static_cast<float4*>(ws);
@@ -400,17 +427,7 @@ size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V) {
 
 const char* fork_last_error(void) { return g_err; }
 
-void fork_release(void) {
-  std::lock_guard<std::mutex> lock(g_ws_mutex);
-  int cur = 0;
-  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
-  for (size_t dev = 0; dev < g_ws.size(); ++dev) {
-    if (!g_ws[dev].ptr) continue;
-    if (hipSetDevice((int)dev) == hipSuccess) (void)hipFree(g_ws[dev].ptr);
-    g_ws[dev] = DeviceWorkspace();
-  }
-  if (have_cur) (void)hipSetDevice(cur);
-}
+void fork_release(void) { g_registry.release_all(); }
 
 int fork_version(void) { return kVersion; }
 

@@ -259,3 +259,25 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
         "    print('raised')\n" % (ROOT, str(tmp_path / "absent.so")))
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
     assert out.returncode == 0 and out.stdout.strip() == "raised", out.stderr
+
+
+def test_workspace_registry_bookkeeping(tmp_path):
+    """The library-managed workspace registry (paper_2609_39859_amd/csrc/
+    workspace_registry.h), compiled for the host with a fake allocator:
+    one buffer per (device, stream), geometric growth that retires the old
+    allocation instead of freeing it under queued work, a failed allocation
+    leaving the previous buffer, concurrent host threads, and release that
+    synchronises every device before freeing."""
+    import shutil
+    import subprocess
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("no host C++ compiler")
+    exe = str(tmp_path / "registry_check")
+    subprocess.run([gxx, "-std=c++17", "-O1", "-Wall", "-Wextra", "-Werror", "-pthread",
+                    "-I", os.path.join(ROOT, "paper_2609_39859_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "native", "registry_check.cpp"), "-o", exe],
+                   check=True)
+    r = subprocess.run([exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    assert "registry ok" in r.stdout

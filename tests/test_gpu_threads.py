@@ -106,3 +106,87 @@ def test_threads_share_managed_workspace():
         for k, (a, b) in enumerate(zip(out, ref)):
             assert torch.equal(a, b), "case %d %s output %d differs from the sequential run" % (ci, name, k)
     _binding.release()
+
+
+def test_streams_get_their_own_managed_workspace():
+    """Two non-default streams (default priority) issue steps of different
+    sizes concurrently on the managed workspace, with no synchronisation
+    between them: each stream has its own buffer, so every result equals the
+    sequential run with a caller workspace, bit for bit."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(DEV)
+    cases = [_case(10 + i, s) for i, s in enumerate(SHAPES)]
+    refs = []
+    for c in cases:
+        ws = _own_workspace(c, _step)
+        off = (-ws.data_ptr()) % 256
+        refs.append([t.clone() for t in _step(c, ws[off:])])
+    torch.cuda.synchronize()
+    _binding.release()
+    streams = [torch.cuda.Stream(DEV), torch.cuda.Stream(DEV)]
+    outs = {0: [], 1: []}
+    for rep in range(3):
+        for si, st in enumerate(streams):
+            with torch.cuda.stream(st):
+                # stream 0 walks the sizes upwards (its buffer grows while
+                # its earlier steps are queued), stream 1 downwards
+                ci = rep if si == 0 else len(cases) - 1 - rep
+                outs[si].append((ci, _step(cases[ci])))
+    torch.cuda.synchronize()
+    for si in (0, 1):
+        for ci, out in outs[si]:
+            for k, (a, b) in enumerate(zip(out, refs[ci])):
+                assert torch.equal(a, b), "stream %d case %d output %d differs" % (si, ci, k)
+    _binding.release()
+
+
+def test_graph_capture_needs_a_caller_workspace():
+    """A step captured into a graph without a workspace of its own is
+    refused (FORK_EINVAL) before anything is enqueued; with a caller
+    workspace it is captured, and each replay (eager state resets and
+    synchronisations in between) gives the eager result."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(DEV)
+    case = _case(20, SHAPES[1])
+    cfg, h, W, tok0, msk0, bs0, _ = case
+    ws = _own_workspace(case, _step)
+    off = (-ws.data_ptr()) % 256
+    ref = [t.clone() for t in _step(case, ws[off:])]
+    torch.cuda.synchronize()
+    M, B = cfg.M, cfg.B
+    f32 = dict(dtype=torch.float32, device=DEV)
+    conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
+    fb = torch.empty(B, dtype=torch.int32, device=DEV)
+    tok, msk, bs = tok0.clone(), msk0.clone(), bs0.clone()
+
+    def step(workspace):
+        _binding.fork_step_ex(h, W, tok, msk, bs, cfg.block_len, float(cfg.tau), conf, ent,
+                              logp, fb, B=B, L=cfg.L, workspace=workspace)
+
+    refused = []
+    g0 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g0):
+        try:
+            step(None)
+        except _binding.ForkError as e:
+            refused.append(e)
+    assert refused and refused[0].code == _binding.FORK_EINVAL, refused
+    assert "captured" in str(refused[0])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(ws[off:])
+    torch.cuda.synchronize()
+    for _ in range(3):
+        tok.copy_(tok0)
+        msk.copy_(msk0)
+        bs.copy_(bs0)
+        for t in (conf, ent, logp):
+            t.fill_(float("nan"))
+        fb.fill_(-9)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, (a, b) in enumerate(zip([conf, ent, logp, fb, tok, msk, bs], ref)):
+            assert torch.equal(a, b), "replay output %d differs from the eager step" % k
