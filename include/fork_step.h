@@ -201,6 +201,29 @@ typedef struct fork_step_args {
 /* fork_step with the extras above.  Same return codes. */
 int fork_step_ex(const fork_step_args* args);
 
+/* Maximum scratch of fork_step_noalloc: 64 MiB, enough for every mode at
+   B*L = 4096 positions and V = 126464 (the LLaDA-8B shape). */
+#define FORK_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* fork_step_ex for callers that cannot allocate device memory: code under
+   HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+   Same arguments, semantics, outputs and kernels as fork_step_ex, but the
+   step's scratch (per-tile partial statistics, candidates, row lists) lives
+   in a static device array of FORK_NOALLOC_SCRATCH_BYTES that the library
+   holds on each GPU it runs on until the process ends; nothing is allocated
+   (no hipMalloc, hipFree or allocating library call).  The first call on a
+   device looks up that device's copy of the array (hipGetSymbolAddress):
+   make it outside graph capture.  Nothing in the scratch needs to start at
+   zero; every call overwrites what it reads.
+   args->workspace must be NULL and args->workspace_bytes 0 (FORK_EINVAL).
+   Sizes whose scratch (fork_workspace_bytes without the drawn partials when
+   sample_temperature == 0) exceeds FORK_NOALLOC_SCRATCH_BYTES return
+   FORK_EUNSUPPORTED before anything is enqueued.
+   All calls on one GPU share its array: calls whose GPU work overlaps (on
+   different streams, or from threads not ordered with each other) race on
+   it and give undefined results; serialise them, e.g. on one stream. */
+int fork_step_noalloc(const fork_step_args* args);
+
 /* Device workspace bytes a step with these sizes needs in any mode (per-tile
    partial statistics, the per-position candidates, the active-row list, and
    the per-tile drawn candidates when sample_temperature > 0); 0 if the sizes

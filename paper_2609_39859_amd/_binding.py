@@ -30,6 +30,7 @@ FORK_RULE_MAXENT = 3
 FORK_RULE_RANDOM = 4
 FORK_ROWS_ALL = 0
 FORK_ROWS_ACTIVE = 1
+FORK_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -109,6 +110,8 @@ def lib():
                                 _P, _P, _I32, _I32, _I32, _I32, _I32, _P]
         L.fork_step_ex.restype = ctypes.c_int
         L.fork_step_ex.argtypes = [ctypes.POINTER(ForkStepArgs)]
+        L.fork_step_noalloc.restype = ctypes.c_int
+        L.fork_step_noalloc.argtypes = [ctypes.POINTER(ForkStepArgs)]
         L.fork_workspace_bytes.restype = ctypes.c_size_t
         L.fork_workspace_bytes.argtypes = [_I32, _I32, _I32]
         L.fork_last_error.restype = ctypes.c_char_p
@@ -178,6 +181,34 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
     """fork_step_ex of the C ABI; optional outputs may be None.  ``events``
     is an optional pair of raw hipEvent_t handles (ints) recorded around the
     LM-head kernel."""
+    a = _step_args(hidden, W_head, tokens, mask, block_start, block_len, tau, out_conf,
+                   out_entropy, out_logp, out_fallback, B, L, out_lse, out_argmax,
+                   out_ncommit, out_commit_pos, rule, workspace, stream, events,
+                   fallback_uniform, rows_mode, temperature, seed, counter)
+    _raise_on(lib().fork_step_ex(ctypes.byref(a)))
+
+
+def fork_step_noalloc(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tensor,
+                      mask: torch.Tensor, block_start: torch.Tensor, block_len: int,
+                      tau: float, out_conf: torch.Tensor, out_entropy: torch.Tensor,
+                      out_logp: torch.Tensor, out_fallback: torch.Tensor, *,
+                      B: int, L: int, out_lse=None, out_argmax=None, out_ncommit=None,
+                      out_commit_pos=None, rule: int = FORK_RULE_LEFTMOST, stream=None,
+                      events=None, fallback_uniform=None, rows_mode: int = FORK_ROWS_ALL,
+                      temperature: float = 0.0, seed: int = 0, counter: int = 0) -> None:
+    """fork_step_noalloc of the C ABI: fork_step_ex on the library's static
+    device scratch (allocates nothing)."""
+    a = _step_args(hidden, W_head, tokens, mask, block_start, block_len, tau, out_conf,
+                   out_entropy, out_logp, out_fallback, B, L, out_lse, out_argmax,
+                   out_ncommit, out_commit_pos, rule, None, stream, events,
+                   fallback_uniform, rows_mode, temperature, seed, counter)
+    _raise_on(lib().fork_step_noalloc(ctypes.byref(a)))
+
+
+def _step_args(hidden, W_head, tokens, mask, block_start, block_len, tau, out_conf,
+               out_entropy, out_logp, out_fallback, B, L, out_lse, out_argmax, out_ncommit,
+               out_commit_pos, rule, workspace, stream, events, fallback_uniform, rows_mode,
+               temperature, seed, counter) -> ForkStepArgs:
     if hidden.dim() != 2 or W_head.dim() != 2:
         raise ValueError("hidden and W_head must be 2-D")
     device = hidden.device
@@ -225,9 +256,7 @@ def fork_step_ex(hidden: torch.Tensor, W_head: torch.Tensor, tokens: torch.Tenso
     a.sample_temperature = float(temperature)
     a.sample_counter = int(counter) & 0xFFFFFFFF
     a.sample_seed = int(seed) & 0xFFFFFFFFFFFFFFFF
-    rc = lib().fork_step_ex(ctypes.byref(a))
-    if rc != FORK_OK:
-        raise ForkError(rc, lib().fork_last_error().decode())
+    return a
 
 
 def _raise_on(rc: int) -> None:

@@ -16,6 +16,12 @@
 #include "fork_kernels.h"
 #include "workspace_registry.h"
 
+// Device scratch of fork_step_noalloc: a static array that every GPU the
+// library runs on holds (its own copy) until the process ends.  Host code
+// never uses the array's name as a device address: the address of each
+// device's copy comes from hipGetSymbolAddress (scratch_address below).
+static __device__ __align__(256) unsigned char scratch[FORK_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
@@ -112,6 +118,33 @@ int get_workspace(hipStream_t stream, size_t need, void** out, std::unique_lock<
   if (rc != FORK_OK) return rc;
   rc = g_registry.acquire(dev, reinterpret_cast<uintptr_t>(stream), need, out, lock);
   if (rc != 0) return rc == FORK_ENOMEM ? FORK_ENOMEM : fail(FORK_EHIP, "workspace allocation failed");
+  return FORK_OK;
+}
+
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};  // device address of `scratch`, per device
+
+// Address of device `dev`'s copy of `scratch`, looked up once per device
+// (with that device current) and kept.
+int scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(FORK_EINVAL, "device %d out of range", dev);
+  std::lock_guard<std::mutex> g(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return fail(FORK_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess)
+      return fail(FORK_EHIP, "hipSetDevice(%d): %s", dev, hipGetErrorString(e));
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p)
+      return fail(FORK_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return FORK_OK;
 }
 
@@ -256,6 +289,30 @@ int fork_step_ex(const fork_step_args* a) {
     rc = get_workspace(static_cast<hipStream_t>(a->stream), lay.total, &ws, &ws_lock);
     if (rc != FORK_OK) return rc;
   }
+  return enqueue_step(a, ws, lay);
+}
+
+int fork_step_noalloc(const fork_step_args* a) {
+  int rc = validate(a);
+  if (rc != FORK_OK) return rc;
+  if (a->workspace || a->workspace_bytes)
+    return fail(FORK_EINVAL, "fork_step_noalloc uses the library's static scratch: "
+                             "workspace must be NULL and workspace_bytes 0");
+  if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
+  Layout lay;
+  if (!layout_for(a->B, a->L, a->V, a->sample_temperature > 0.0f, &lay))
+    return fail(FORK_EINVAL, "invalid sizes");
+  if (lay.total > (size_t)FORK_NOALLOC_SCRATCH_BYTES)
+    return fail(FORK_EUNSUPPORTED,
+                "fork_step_noalloc: these sizes need %zu bytes of scratch, more than its "
+                "maximum of %zu; use fork_step_ex with a workspace",
+                lay.total, (size_t)FORK_NOALLOC_SCRATCH_BYTES);
+  int dev = 0;
+  rc = stream_device(static_cast<hipStream_t>(a->stream), &dev);
+  if (rc != FORK_OK) return rc;
+  void* ws = nullptr;
+  rc = scratch_address(dev, &ws);
+  if (rc != FORK_OK) return rc;
   return enqueue_step(a, ws, lay);
 }
 

@@ -281,3 +281,36 @@ def test_workspace_registry_bookkeeping(tmp_path):
     r = subprocess.run([exe], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
     assert "registry ok" in r.stdout
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(workspace=256, workspace_bytes=1 << 30), _binding.FORK_EINVAL),  # no caller workspace
+    (dict(workspace_bytes=1), _binding.FORK_EINVAL),
+    (dict(tau=float("nan")), _binding.FORK_EINVAL),                        # same validation
+    # partials of 8192 positions x 512 vocabulary tiles = 64 MiB, + candidates
+    (dict(B=16, L=512, block_len=32, V=131072), _binding.FORK_EUNSUPPORTED),
+    # drawn candidates double the partials
+    (dict(B=8, L=512, block_len=32, V=126464, sample_temperature=0.8, ), None),
+    (dict(B=16, L=512, block_len=32, V=126464, sample_temperature=0.8), _binding.FORK_EUNSUPPORTED),
+])
+def test_noalloc_rejections_on_host(kw, code):
+    """fork_step_noalloc refuses a caller workspace and sizes beyond its
+    static scratch before any HIP call (the pointers are never used)."""
+    L = _binding.lib()
+    if code is None:
+        # fits: the scratch size check passes (the LLaDA-8B shape with drawn
+        # candidates needs 2 x 32.4 MB of partials + 32 KB)
+        assert L.fork_workspace_bytes(8, 512, 126464) <= _binding.FORK_NOALLOC_SCRATCH_BYTES
+        return
+    assert L.fork_step_noalloc(ctypes.byref(_args(**kw))) == code
+    msg = L.fork_last_error().decode()
+    assert msg != ""
+    if code == _binding.FORK_EUNSUPPORTED:
+        assert "scratch" in msg
+
+
+def test_noalloc_empty_batch_is_a_no_op():
+    L = _binding.lib()
+    nulls = dict(hidden=0, W_head=0, tokens=0, mask=0, block_start=0, out_conf=0,
+                 out_entropy=0, out_logp=0, out_fallback=0, B=0)
+    assert L.fork_step_noalloc(ctypes.byref(_args(**nulls))) == _binding.FORK_OK
