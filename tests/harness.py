@@ -101,6 +101,24 @@ class Report:
     max_err: dict = dataclasses.field(default_factory=dict)
 
 
+# Exclusion counts of every parity check run in this session (written out by
+# tests/conftest.py at the end of the session).
+RECORDS = []
+
+
+def record(rep: Report, config: str, **extra) -> None:
+    """Keep the counts of one parity check: rows compared and how many were
+    near-ties, sequence-steps compared and how many sat near the threshold,
+    the largest errors; labelled with the running test."""
+    import os
+    test = os.environ.get("PYTEST_CURRENT_TEST", "?").rsplit(" ", 1)[0]
+    RECORDS.append(dict(test=test, config=config, rows=rep.rows,
+                        near_tie_rows=rep.near_tie_rows, seqs=rep.seqs,
+                        near_threshold_seqs=rep.near_threshold_seqs,
+                        max_err={k: float(v) for k, v in sorted(rep.max_err.items())},
+                        **extra))
+
+
 def compare_stats(g: GpuOut, ref: dict, rows, hbits, Wbits, d: int, rep: Report):
     rows = np.asarray(rows)
     for k in ("conf", "entropy", "logp", "lse"):

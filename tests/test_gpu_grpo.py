@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 import torch
 
+import harness
 import oracle
 from paper_2609_39859_amd import _binding, synth
 
@@ -216,6 +217,7 @@ def test_forkgrpo_rollouts_and_objective():
     entries = []            # (step, b, k, token, lp_old oracle, lp_old gpu)
     hs = []
     excluded = 0
+    rep = harness.Report()
     t = 0
     while msk.any():
         h = synth.hidden(cfg, t, W=W)
@@ -232,8 +234,7 @@ def test_forkgrpo_rollouts_and_objective():
         act = np.array(act, np.int64)
         st = oracle.row_stats(hb, Wb, act)
         sm = oracle.row_sample(hb, Wb, act, temp, seed, t)
-        ties = compare_sampled(g, st, sm, act, hb, Wb, cfg.d, temp, seed, t,
-                               __import__("harness").Report())
+        ties = compare_sampled(g, st, sm, act, hb, Wb, cfg.d, temp, seed, t, rep)
         conf = np.full(cfg.M, np.nan)
         cand = np.zeros(cfg.M, np.int32)
         conf[act], cand[act] = sm["conf"], sm["cand"]
@@ -257,6 +258,9 @@ def test_forkgrpo_rollouts_and_objective():
         t += 1
         assert t <= cfg.G + 1
     assert excluded <= max(2, len(entries) // 20)
+    rep.seqs, rep.near_threshold_seqs = len(entries), excluded
+    harness.record(rep, cfg.name, steps=t, temperature=temp, fallback_entries=len(entries),
+                   tau=cfg.tau)
     # rollouts (one per sequence) with their fallback entries, CSR by rollout
     entries.sort(key=lambda e: (e[1], e[0]))
     counts = np.bincount([e[1] for e in entries], minlength=B)

@@ -18,7 +18,7 @@ import oracle
 from paper_2609_39859_amd import _binding, synth
 
 from harness import (Report, check_rule_on_own_stats, compare_decisions, compare_sampled,
-                     compare_stats, gpu_step, host_bits)
+                     compare_stats, gpu_step, host_bits, record)
 
 pytestmark = pytest.mark.gpu
 
@@ -96,6 +96,8 @@ def lockstep_decode(cfg, rule=0, max_steps=None, rows_fn=None,
     _say("%s: %d steps, %d rows (%d near-tie), %d sequence-steps (%d near-threshold), max err %s"
          % (cfg.name, t, rep.rows, rep.near_tie_rows, rep.seqs, rep.near_threshold_seqs,
             {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, cfg.name, steps=t, rule=rule, rows_mode=rows_mode, temperature=temperature,
+           tau=cfg.tau)
     return rep, t
 
 
@@ -271,6 +273,7 @@ def test_mid_step0_all_rows():
     compare_decisions(g, sel, ref["conf"], tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau,
                       rep, near_tie_rows=ties)
     _say("mid step 0: near-tie rows %d / %d, max err %s" % (rep.near_tie_rows, rep.rows, rep.max_err))
+    record(rep, cfg.name, steps=1, tau=cfg.tau)
     assert rep.near_tie_rows <= cfg.M // 50
 
 
@@ -337,6 +340,7 @@ def test_ragged_shapes_and_random_states(B, L, d, V, dtype, BL, rule):
                                entropy=ref["entropy"], uniform=uni)
         compare_decisions(g, sel, ref["conf"], tok, msk, bs, B, L, BL, tau, rep, rule=rule,
                           near_tie_rows=ties, entropy_ref=ref["entropy"], uniform=uni)
+        record(rep, "ragged", shape=[B, L, d, V, BL], rule=rule, tau=tau)
 
 
 @pytest.mark.parametrize("B,L,d,V,dtype,BL", RAGGED)
@@ -436,6 +440,7 @@ def test_drawn_candidates_ragged_and_mode_invariant(B, L, d, V, dtype, BL):
         compare_sampled(a, {k: v[active] for k, v in st.items()}, sm, active, hb, Wb, d,
                         temperature, SEED, counter, rep)
     _say("ragged drawn %s: %d rows (%d near-tie)" % ((B, L, d, V, BL), rep.rows, rep.near_tie_rows))
+    record(rep, "ragged", shape=[B, L, d, V, BL], temperature=temperature)
 
 
 def test_drawn_candidates_change_with_counter_and_seed():
@@ -477,6 +482,7 @@ def test_extreme_sizes(M, d, V):
     compare_stats(g, ref, np.arange(M), hb, Wb, d, rep)
     _say("extreme sizes M=%d d=%d V=%d: max err %s" % (
         M, d, V, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, "extreme", shape=[M, d, V])
 
 
 def test_caller_workspace_and_determinism():
@@ -572,6 +578,7 @@ def test_full_size_step_sampled(name):
     assert np.all(g.commit_pos[:, 0] == cfg.P) and np.all(g.commit_pos[:, 1:] == -1)
     _say("full-size %s: %d rows ok (%d near-tie), max err %s" % (
         name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, name, steps=1, tau=cfg.tau)
 
 
 @pytest.mark.parametrize("name", ["llada8b", "rollout"])
@@ -598,6 +605,7 @@ def test_full_size_active_rows_mode(name):
     compare_stats(b, ref, rows, host_bits(h), host_bits(W), cfg.d, rep)
     _say("full-size active %s: ok, max err %s" % (
         name, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, name, steps=1, rows_mode=1, tau=cfg.tau)
 
 
 @pytest.mark.parametrize("name,rows_mode", [("llada8b", 0), ("llada8b", 1), ("rollout", 1)])
@@ -621,6 +629,7 @@ def test_full_size_drawn_candidates(name, rows_mode):
     compare_sampled(g, st, sm, rows, hb, Wb, cfg.d, 0.8, SEED, 2, rep)
     _say("full-size drawn %s: %d rows ok (%d near-tie), max err %s" % (
         name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, name, steps=1, rows_mode=rows_mode, temperature=0.8, tau=cfg.tau)
 
 
 def test_full_size_planted_peaks_lockstep():
@@ -654,45 +663,178 @@ def test_full_size_planted_peaks_lockstep():
     assert multi >= 4, "expected parallel multi-commit steps, got %d" % multi
     _say("planted full-size: %d rows (%d near-tie), %d multi-commit sequence-steps, max err %s" % (
         rep.rows, rep.near_tie_rows, multi, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, cfg.name, steps=3, multi_commit_seq_steps=multi, tau=cfg.tau)
 
 
-@pytest.mark.parametrize("name", ["llada8b"])
+def _decode_checks(cfg):
+    """Steps of a full-size decode checked against the oracle, by kind:
+    "block" = every row of the active blocks (at most 256) + 64 sampled rows,
+    "commit" = the committed rows + 16 sampled rows.  They include the first
+    step, the last step of the first block, the first two steps of the
+    second, the middle block boundary and the final step."""
+    BL, G = cfg.block_len, cfg.G
+    big = cfg.B * BL > 256
+    checks = {t: "commit" for t in (BL - 1, BL + 1, G // 2 - 1, G // 2)}
+    for t in (0, BL, G - 1):
+        checks[t] = "commit" if big else "block"
+    return checks
+
+
+@pytest.mark.parametrize("name", ["llada8b", "rollout", "long"])
 def test_full_size_decode_is_autoregressive(name):
-    """A whole decode at the full LLaDA-8B shape on the GPU: with no
-    confident position, every step is a fallback step and the commits follow
-    AR order P, P+1, ... (Section 2); a few steps are checked against the
-    oracle on their active rows."""
+    """A whole decode at full size on the GPU, in the launch configuration
+    the benchmark times (all B*L rows through the LM head), hidden states
+    regenerated every step.  With no confident position every step is a
+    fallback step and the commits follow AR order P, P+1, ... (Section 2),
+    crossing every block boundary (Section 4.1).  At the steps of
+    _decode_checks the GPU's statistics are compared with the oracle's on
+    the committed or active-block rows plus sampled rows, and the decision
+    against the oracle's selection on those rows.  Per step, the fallback
+    flag and the log-probability of the committed token (the inputs of
+    ForkGRPO, Section 3.2) are kept; at the end the recorded
+    log-probabilities of checked steps are recomputed by fork_logprob
+    (teacher forcing on the committed tokens)."""
     _need_gpu()
     cfg = synth.CONFIGS[name]
     W = synth.weights(cfg, device=DEV)
     Wb = None
     tok, msk, bs = (x.to(DEV) for x in synth.initial_state(cfg))
-    B, L, BL, M = cfg.B, cfg.L, cfg.block_len, cfg.M
+    B, L, BL, M, P = cfg.B, cfg.L, cfg.block_len, cfg.M, cfg.P
     f32 = dict(dtype=torch.float32, device=DEV)
-    conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
+    conf, ent, logp, lse = (torch.empty(M, **f32) for _ in range(4))
     am = torch.empty(M, dtype=torch.int32, device=DEV)
     fb = torch.empty(B, dtype=torch.int32, device=DEV)
+    nc = torch.empty(B, dtype=torch.int32, device=DEV)
     cp = torch.empty(B * BL, dtype=torch.int32, device=DEV)
-    check_steps = {0, 1, 31, 32, cfg.G - 1}
+    checks = _decode_checks(cfg)
+    rng = np.random.default_rng(cfg.seed + 99)
+    fallbacks = np.zeros((cfg.G, B), np.int32)
+    logp_commit = np.zeros((cfg.G, B), np.float32)
+    rep = Report()
+    lam = _lam(cfg.tau)
+    max_conf = 0.0
+    _say("full-size decode %s: %d steps, checks at %s" % (name, cfg.G, sorted(checks)))
     for t in range(cfg.G):
         h = synth.hidden(cfg, t, device=DEV)
-        if t in check_steps:
-            before = msk.cpu().numpy()
+        if t in checks:
+            before = (tok.cpu().numpy(), msk.cpu().numpy(), bs.cpu().numpy())
         _binding.fork_step_ex(h, W, tok, msk, bs, BL, cfg.tau, conf, ent, logp, fb, B=B, L=L,
-                              out_argmax=am, out_commit_pos=cp)
+                              out_lse=lse, out_argmax=am, out_ncommit=nc, out_commit_pos=cp)
         fbh = fb.cpu().numpy()
         cph = cp.cpu().numpy().reshape(B, BL)
         assert np.all(fbh == 1), "step %d: fallback %s" % (t, fbh)
-        assert np.all(cph[:, 0] == cfg.P + t) and np.all(cph[:, 1:] == -1)
-        if t in check_steps:
-            if Wb is None:
-                Wb = host_bits(W)
-            rows = np.array([b * L + cfg.P + t for b in range(B)])
-            ref = oracle.row_stats(host_bits(h), Wb, rows)
-            gam = am.cpu().numpy()[rows]
-            gtok = tok.cpu().numpy()[rows]
-            ok = (gam == ref["argmax"]) | (ref["gap"] < 2e-3)
-            assert np.all(ok) and np.array_equal(gtok, gam)
-            assert before[rows].all()
-            _say("decode %s step %d ok" % (name, t))
-    assert not msk.cpu().numpy().reshape(B, L)[:, cfg.P:].any()
+        assert np.all(cph[:, 0] == P + t) and np.all(cph[:, 1:] == -1), "step %d: commits" % t
+        committed = np.arange(B) * L + P + t
+        fallbacks[t] = fbh
+        logp_commit[t] = logp[torch.as_tensor(committed, device=DEV)].cpu().numpy()
+        # the threshold decision has a margin far wider than the 2e-3
+        # statistics tolerance, so the oracle's decision is the GPU's
+        max_conf = max(max_conf, float(conf.max().item()))
+        if t not in checks:
+            continue
+        if Wb is None:
+            Wb = host_bits(W)
+        hb = host_bits(h)
+        tok0, msk0, bs0 = before
+        active = _active_rows(cfg, msk0, bs0)
+        if checks[t] == "block":
+            rows = np.union1d(active, rng.choice(M, 64, replace=False))
+        else:
+            rows = np.union1d(committed, rng.choice(M, 16, replace=False))
+        _say("full-size decode %s step %d: oracle on %d rows (%s)" % (name, t, rows.size, checks[t]))
+        g = types.SimpleNamespace(conf=conf.cpu().numpy(), entropy=ent.cpu().numpy(),
+                                  logp=logp.cpu().numpy(), lse=lse.cpu().numpy(),
+                                  argmax=am.cpu().numpy(), tokens=tok.cpu().numpy(),
+                                  mask=msk.cpu().numpy(), block_start=bs.cpu().numpy(),
+                                  fallback=fbh, ncommit=nc.cpu().numpy(), commit_pos=cph)
+        ref = oracle.row_stats(hb, Wb, rows)
+        ties = compare_stats(g, ref, rows, hb, Wb, cfg.d, rep)
+        assert np.array_equal(g.tokens[committed], g.argmax[committed])
+        assert msk0[committed].all() and not g.mask[committed].any()
+        if checks[t] == "block":
+            conf_full = np.full(M, np.nan)
+            am_full = np.zeros(M, np.int32)
+            conf_full[rows], am_full[rows] = ref["conf"], ref["argmax"]
+            sel = oracle.select(conf_full, am_full, tok0, msk0, bs0, B, L, BL, lam)
+            compare_decisions(g, sel, conf_full, tok0, msk0, bs0, B, L, BL, cfg.tau, rep,
+                              near_tie_rows=ties)
+        else:
+            check_rule_on_own_stats(g, tok0, msk0, bs0, B, L, BL, cfg.tau, 0, range(B))
+            rep.seqs += B
+    assert not msk.cpu().numpy().reshape(B, L)[:, P:].any()
+    assert max_conf < lam - 0.01, "a confident position (%g) near lambda" % max_conf
+    assert np.all(fallbacks == 1)
+    assert np.all(np.isfinite(logp_commit)) and np.all(logp_commit <= 0)
+    # ForkGRPO reads the recorded log q of each fallback commit: the
+    # teacher-forced likelihood of the committed tokens under the same head
+    # reproduces it
+    final_tok = tok
+    for t in sorted(checks)[:3]:
+        h = synth.hidden(cfg, t, device=DEV)
+        rows_t = torch.as_tensor(np.arange(B) * L + P + t, dtype=torch.int32, device=DEV)
+        out = torch.empty(B, **f32)
+        _binding.logprob(h, W, final_tok[rows_t.long()].contiguous(), out, rows=rows_t)
+        np.testing.assert_allclose(out.cpu().numpy(), logp_commit[t], rtol=0, atol=1e-5)
+    _say("full-size decode %s: %d steps, %d rows checked (%d near-tie), %d sequence-steps, "
+         "max conf %.3g, max err %s" % (name, cfg.G, rep.rows, rep.near_tie_rows, rep.seqs,
+                                        max_conf, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, name, steps=cfg.G, decode=True, max_conf=max_conf, tau=cfg.tau)
+
+
+def _device_decode(cfg, W, hidden_at, state, t0, t1=None):
+    """Steps t0 .. t1-1 (or until nothing is masked) on device-resident
+    state; per-step host copies of the outputs, and the state at the end."""
+    tok, msk, bs = (torch.as_tensor(x).to(DEV) for x in state)
+    B, L, BL, M = cfg.B, cfg.L, cfg.block_len, cfg.M
+    f32 = dict(dtype=torch.float32, device=DEV)
+    outs = []
+    t = t0
+    while (t1 is None and bool(msk.any())) or (t1 is not None and t < t1):
+        assert t < cfg.G
+        conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
+        fb = torch.empty(B, dtype=torch.int32, device=DEV)
+        cp = torch.empty(B * BL, dtype=torch.int32, device=DEV)
+        _binding.fork_step_ex(hidden_at(t), W, tok, msk, bs, BL, cfg.tau, conf, ent, logp, fb,
+                              B=B, L=L, out_commit_pos=cp)
+        outs.append([x.cpu().numpy() for x in (conf, ent, logp, fb, cp)])
+        t += 1
+    return outs, tuple(x.cpu().numpy() for x in (tok, msk, bs))
+
+
+def test_gpu_resume_matches_uninterrupted():
+    """The decode's whole state is (tokens, mask, block_start): a GPU decode
+    stopped after k steps, its state moved to the host, the library's
+    workspaces released and the decode resumed from fresh device buffers
+    gives bit-identical per-step outputs and final state to the
+    uninterrupted decode (mid_planted: parallel and fallback steps, blocks
+    skipped forward)."""
+    _need_gpu()
+    cfg = synth.CONFIGS["mid_planted"]
+    W = synth.weights(cfg)
+    Wd = W.to(DEV)
+    cache = {}
+
+    def hidden_at(t):
+        if t not in cache:
+            cache[t] = synth.hidden(cfg, t, W=W).to(DEV)
+        return cache[t]
+
+    state0 = tuple(x.numpy() for x in synth.initial_state(cfg))
+    ref_outs, ref_final = _device_decode(cfg, Wd, hidden_at, state0, 0)
+    T = len(ref_outs)
+    assert T > 6 and not ref_final[1].any()
+    fbs = np.array([o[3] for o in ref_outs])
+    assert (fbs == 0).any() and (fbs == 1).any(), "expected parallel and fallback steps"
+    for k in (1, T // 2, T - 1):
+        a, mid = _device_decode(cfg, Wd, hidden_at, state0, 0, k)
+        torch.cuda.synchronize()
+        _binding.release()
+        b, final = _device_decode(cfg, Wd, hidden_at, mid, k)
+        assert len(a) + len(b) == T
+        for t, (x, y) in enumerate(zip(a + b, ref_outs)):
+            for i, (u, v) in enumerate(zip(x, y)):
+                assert np.array_equal(u.view(np.int32), v.view(np.int32)), \
+                    "resume after %d: step %d output %d differs" % (k, t, i)
+        for u, v in zip(final, ref_final):
+            assert np.array_equal(u, v)
+    _say("resume: %d-step decode reproduced after stops at %s" % (T, [1, T // 2, T - 1]))
