@@ -21,6 +21,14 @@ log-probabilities plus its objective; `selection` gives the unmasking
 rule's latency at the real shapes and its HBM bandwidth on a sweep of large
 batches; `measured_peaks` gives this GPU's achievable MFMA and HBM rates
 (probe kernels), and the rooflines also quote fractions of those.
+`configs` times the other workloads of the benchmark definition (mid
+B=4 L=256 d=1024 V=32000; rollout B=64 L=384; long B=2 L=2048 block 64),
+each eagerly and as a captured HIP graph of the same steps; `cpu_baseline`
+carries further legs (one thread and all threads, full steps of the tiny and
+mid workloads, the host's CPU model); `context_unfused_torch` times the
+same LLaDA-8B-shaped step done by unfused torch operations (library GEMM
+writing the logits, then reductions and a tensor-level selection), for
+context only.
 """
 import argparse
 import ctypes
@@ -73,6 +81,21 @@ def _traffic_per_launch(kernel):
     return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_threads():
+    return int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0)) or 1
+
+
 def cpu_baseline(cfg, W_dev, h_dev, target_s):
     """Time the oracle (as it is) on a bounded sample of rows of this
     workload; scale rows/s to steps/s (a step covers B*L rows)."""
@@ -82,7 +105,7 @@ def cpu_baseline(cfg, W_dev, h_dev, target_s):
     from paper_2609_39859_amd import synth
     Wb = synth.to_bits(W_dev)
     hb = synth.to_bits(h_dev)
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count() or 1
+    threads = _oracle_threads()
     orc = oracle.default()
     probe = np.arange(threads, dtype=np.int64)
     t0 = time.perf_counter()
@@ -95,10 +118,57 @@ def cpu_baseline(cfg, W_dev, h_dev, target_s):
     dt = time.perf_counter() - t0
     assert np.all(np.isfinite(st["conf"]))
     rows_per_s = rows.size / dt
+    # the same workload on one thread, a few rows
+    rows1 = np.arange(4, dtype=np.int64)
+    t0 = time.perf_counter()
+    orc.row_stats(hb, Wb, rows1, nthreads=1)
+    dt1 = time.perf_counter() - t0
     return {"value": rows_per_s / cfg.M, "unit": "steps/s", "cores": threads, "kind": "oracle",
             "sample": "%d of the %d rows of one step (binary64 logits over all %d vocabulary "
                       "entries + statistics), %.1f s on %d threads; value = rows/s / %d"
-                      % (rows.size, cfg.M, cfg.V, dt, threads, cfg.M)}
+                      % (rows.size, cfg.M, cfg.V, dt, threads, cfg.M),
+            "cpu_model": _cpu_model(), "host_cpus": len(os.sched_getaffinity(0)),
+            "one_thread": {"value": rows1.size / dt1 / cfg.M, "unit": "steps/s",
+                           "sample": "%d rows, %.1f s on 1 thread" % (rows1.size, dt1)}}
+
+
+def cpu_legs():
+    """Further oracle timings: whole steps (statistics of every row, then
+    the selection) of the tiny and mid workloads on one thread and on all
+    threads; the mid step on one thread is timed on a sample of rows and
+    scaled (marked so)."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_39859_amd import synth
+    threads = _oracle_threads()
+    orc = oracle.default()
+    out = {"cpu_model": _cpu_model(), "threads": threads, "legs": []}
+    for name in ("tiny", "mid"):
+        cfg = synth.CONFIGS[name]
+        W = synth.to_bits(synth.weights(cfg))
+        h = synth.to_bits(synth.hidden(cfg, 0))
+        tok, msk, bs = (x.numpy() for x in synth.initial_state(cfg))
+        lam = float(np.float32(cfg.tau))
+        for nt in (1, threads):
+            if name == "mid" and nt == 1:
+                rows = np.arange(0, cfg.M, 16, dtype=np.int64)   # 64 of 1024 rows
+                t0 = time.perf_counter()
+                orc.row_stats(h, W, rows, nthreads=1)
+                dt = (time.perf_counter() - t0) * cfg.M / rows.size
+                how = "rows %d of %d timed, scaled to the whole step" % (rows.size, cfg.M)
+            else:
+                reps, t0 = 0, time.perf_counter()
+                while True:
+                    orc.step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, lam, nthreads=nt)
+                    reps += 1
+                    if time.perf_counter() - t0 > 0.5:
+                        break
+                dt = (time.perf_counter() - t0) / reps
+                how = "%d whole steps" % reps
+            out["legs"].append({"workload": name, "threads": nt, "s_per_step": dt,
+                                "steps_per_s": 1.0 / dt, "how": how})
+    return out
 
 
 def grpo_likelihood(args, hip, W, h, dev):
@@ -217,30 +287,42 @@ def selection(args, dev):
     LLaDA-8B shape, so every step is a fallback step committing one
     position): algorithmic bytes per sequence = block start, the block's 32
     mask bytes and 32 confidences read, the committed candidate read, and
-    token, mask byte, fallback flag and block start written."""
+    token, mask byte, fallback flag and block start written.  The timed
+    launches cycle over enough distinct copies of the batch that together
+    they exceed twice the 256 MB last-level cache, so the bytes come from
+    HBM, not from the cache."""
     import torch
 
     from paper_2609_39859_amd import _binding
     out = {"latency_us": {}, "sweep": []}
 
-    def run(B, L, BL, reps, warmup):
-        gen = torch.Generator(device=dev).manual_seed(B + L)
+    def make(B, L, seed):
+        gen = torch.Generator(device=dev).manual_seed(seed)
         M = B * L
-        conf = torch.rand(M, generator=gen, device=dev) * 0.03
-        am = torch.randint(0, 126464, (M,), generator=gen, device=dev, dtype=torch.int32)
-        tok = torch.full((M,), -1, dtype=torch.int32, device=dev)
-        msk = torch.ones(M, dtype=torch.uint8, device=dev)
-        bs = torch.zeros(B, dtype=torch.int32, device=dev)
-        fb = torch.empty(B, dtype=torch.int32, device=dev)
-        for _ in range(warmup):
-            _binding.select(conf, am, tok, msk, bs, BL, 0.9, fb, B=B, L=L)
+        return dict(conf=torch.rand(M, generator=gen, device=dev) * 0.03,
+                    am=torch.randint(0, 126464, (M,), generator=gen, device=dev, dtype=torch.int32),
+                    tok=torch.full((M,), -1, dtype=torch.int32, device=dev),
+                    msk=torch.ones(M, dtype=torch.uint8, device=dev),
+                    bs=torch.zeros(B, dtype=torch.int32, device=dev),
+                    fb=torch.empty(B, dtype=torch.int32, device=dev))
+
+    def run(B, L, BL, reps, warmup, nsets=1):
+        sets = [make(B, L, B + L + k) for k in range(nsets)]
+
+        def launch(x):
+            _binding.select(x["conf"], x["am"], x["tok"], x["msk"], x["bs"], BL, 0.9, x["fb"],
+                            B=B, L=L)
+        for k in range(warmup):
+            launch(sets[k % nsets])
         torch.cuda.synchronize()
         # the timed launches replay as one HIP graph, so host launch
         # overhead does not separate them (the call allocates nothing)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            for _ in range(reps):
-                _binding.select(conf, am, tok, msk, bs, BL, 0.9, fb, B=B, L=L)
+            for k in range(reps):
+                launch(sets[k % nsets])
+        torch.cuda.synchronize()
+        graph.replay()  # untimed first replay
         torch.cuda.synchronize()
         start = torch.cuda.Event(enable_timing=True)
         stop = torch.cuda.Event(enable_timing=True)
@@ -248,19 +330,240 @@ def selection(args, dev):
         graph.replay()
         stop.record()
         torch.cuda.synchronize()
-        assert int((fb == 1).sum().item()) == B
-        assert int(msk.view(B, L)[:, :warmup + reps].sum().item()) == 0
+        # every launch committed one position of each sequence
+        per_set = [warmup // nsets + (1 if k < warmup % nsets else 0) +
+                   2 * (reps // nsets + (1 if k < reps % nsets else 0)) for k in range(nsets)]
+        for x, n in zip(sets, per_set):
+            assert int((x["fb"] == 1).sum().item()) == B
+            assert int(x["msk"].view(B, L)[:, :n].sum().item()) == 0
+            assert int(x["msk"].view(B, L)[:, n:].sum().item()) == B * (L - n)
         return start.elapsed_time(stop) * 1e3 / reps
 
     for name, B, L, BL in (("llada8b", 8, 512, 32), ("rollout", 64, 384, 32),
                            ("long", 2, 2048, 64)):
         out["latency_us"][name] = run(B, L, BL, 20, 3)
+    set_bytes_per_seq = 32 * (4 + 4 + 4 + 1) + 4 + 4  # conf, candidates, tokens, mask, state
     for B in (1 << 14, 1 << 17, 1 << 20):
-        us = run(B, 32, 32, 20, 3)   # 23 steps commit positions 0..22 of 32
+        nsets = max(1, -(-(512 << 20) // (set_bytes_per_seq * B)))
+        reps = max(20, nsets)
+        assert 3 + 2 * -(-reps // nsets) < 32   # each copy keeps masked positions
+        us = run(B, 32, 32, reps, 3, nsets)
         gbs = SEL_BYTES_PER_SEQ * B / (us * 1e-6) / 1e9
         out["sweep"].append({"B": B, "L": 32, "block_len": 32, "us": us, "GB_s": gbs,
                              "frac_hbm": gbs / PEAK_HBM_GBS,
-                             "bytes_per_seq": SEL_BYTES_PER_SEQ})
+                             "bytes_per_seq": SEL_BYTES_PER_SEQ, "batch_copies": nsets,
+                             "bytes_cycled": nsets * set_bytes_per_seq * B})
+    return out
+
+
+def context_unfused_torch(cfg, W, h, state, dev, steps):
+    """Context only: the same step done by unfused torch operations on the
+    same GPU and inputs.  The library GEMM (torch's linear, hipBLASLt)
+    writes the [B*L, V] logits; fp32 log-sum-exp, maximum and entropy follow
+    as separate reductions; the selection is done with tensor operations
+    over the sequences' active blocks.  Also times the library GEMM alone."""
+    import torch
+    import torch.nn.functional as F
+    B, L, BL, M, V = cfg.B, cfg.L, cfg.block_len, cfg.M, cfg.V
+    tok0, msk0, bs0 = (x.to(dev) for x in state)
+    tok, msk, bs = tok0.clone(), msk0.clone(), bs0.clone()
+    pos = torch.arange(L, device=dev)
+    tau = float(cfg.tau)
+
+    def gemm():
+        return F.linear(h, W)
+
+    def step():
+        z = F.linear(h, W).float()
+        lse = torch.logsumexp(z, dim=1)
+        zmax, am = z.max(dim=1)
+        p = torch.exp(z - lse[:, None])
+        ent = lse - (p * z).sum(dim=1)
+        conf = torch.exp(zmax - lse)
+        logp = zmax - lse
+        m2 = msk.view(B, L).bool()
+        cand = m2 & (pos[None, :] >= bs[:, None])
+        has = cand.any(dim=1)
+        first = torch.where(has, cand.int().argmax(dim=1), torch.full_like(bs, L))
+        s = bs + torch.div(first - bs, BL, rounding_mode="floor") * BL
+        inblk = cand & (pos[None, :] >= s[:, None]) & (pos[None, :] < (s + BL)[:, None])
+        passing = inblk & (conf.view(B, L) > tau)
+        fb = ~passing.any(dim=1)
+        commit = torch.where(fb[:, None], inblk & (pos[None, :] == first[:, None]), passing)
+        tv = tok.view(B, L)
+        tv[commit] = am.view(B, L).int()[commit]
+        m2v = msk.view(B, L)
+        m2v[commit] = 0
+        bs.copy_(torch.where(has, s, bs))
+        return ent, logp
+
+    def timeit(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    gemm_ms = timeit(gemm, steps)
+    step_ms = timeit(step, steps)
+    # the torch step commits what the library commits (all-fallback here)
+    assert bool((msk.view(B, L)[:, cfg.P:cfg.P + steps + 1] == 0).all())
+    flops = 2.0 * M * cfg.d * V
+    return {"library_gemm_ms": gemm_ms,
+            "library_gemm_TFLOP_s": flops / (gemm_ms * 1e-3) / 1e12,
+            "unfused_step_ms": step_ms, "unfused_steps_per_s": 1000.0 / step_ms,
+            "how": "torch linear (hipBLASLt) bf16 logits [B*L, V], then fp32 logsumexp, max, "
+                   "entropy and a tensor-level selection; %d steps" % steps}
+
+
+class StepBench:
+    """Decode steps of one workload on inputs resident in HBM: the
+    weights, a few batches of hidden states used in turn, the decode state
+    and the outputs."""
+
+    def __init__(self, cfg, dev, hip, n_batches=4):
+        import torch
+
+        from paper_2609_39859_amd import synth
+        self.cfg, self.dev, self.hip = cfg, dev, hip
+        self.W = synth.weights(cfg, device=dev)
+        self.hs = [synth.hidden(cfg, t, device=dev,
+                                W=self.W if cfg.plant_peaks > 0 else None)
+                   for t in range(n_batches)]
+        self.state0 = synth.initial_state(cfg)
+        self.tok, self.msk, self.bs = (x.to(dev) for x in self.state0)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.conf, self.ent, self.logp = (torch.empty(cfg.M, **f32) for _ in range(3))
+        self.fb = torch.empty(cfg.B, dtype=torch.int32, device=dev)
+
+    def reset(self):
+        import torch
+        for d, s in zip((self.tok, self.msk, self.bs), self.state0):
+            d.copy_(s.to(self.dev))
+        torch.cuda.synchronize()
+
+    def step(self, i, events=None, rows_mode=0, temperature=0.0, workspace=None):
+        from paper_2609_39859_amd import _binding
+        c = self.cfg
+        _binding.fork_step_ex(self.hs[i % len(self.hs)], self.W, self.tok, self.msk, self.bs,
+                              c.block_len, c.tau, self.conf, self.ent, self.logp, self.fb,
+                              B=c.B, L=c.L, events=events, rows_mode=rows_mode,
+                              temperature=temperature, seed=0x5EED, counter=i,
+                              workspace=workspace)
+
+    def timed(self, rows_mode, steps, warmup, temperature=0.0):
+        """Warm up, restart the decode, then time `steps` steps: total time
+        from torch events on the current stream, LM-head time per step from
+        HIP events the library records around that kernel on the same
+        stream."""
+        import torch
+        hip = self.hip
+        evs = []
+        for _ in range(2 * steps):
+            e = ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(e)) == 0
+            evs.append(e.value)
+        for i in range(warmup):
+            self.step(i, rows_mode=rows_mode, temperature=temperature)
+        torch.cuda.synchronize()
+        self.reset()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        start.record()
+        for i in range(steps):
+            self.step(i, (evs[2 * i], evs[2 * i + 1]), rows_mode=rows_mode,
+                      temperature=temperature)
+        stop.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        lm = []
+        for i in range(steps):
+            ms = ctypes.c_float()
+            assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
+            lm.append(ms.value)
+        for e in evs:
+            hip.hipEventDestroy(e)
+        return start.elapsed_time(stop), lm, wall
+
+    def graph_timed(self, steps, rows_mode=0):
+        """The same `steps` steps captured into one HIP graph (caller
+        workspace) and replayed: the GPU's time per step without host
+        launch gaps.  The replayed decode must end in the state the eager
+        steps reach."""
+        import torch
+
+        from paper_2609_39859_amd import _binding
+        c = self.cfg
+        nbytes = _binding.workspace_bytes(c.B, c.L, c.V)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.dev)
+        off = (-buf.data_ptr()) % 256
+        ws = buf[off:off + nbytes]
+        self.reset()
+        for i in range(steps):
+            self.step(i, rows_mode=rows_mode, workspace=ws)
+        torch.cuda.synchronize()
+        want = (self.tok.clone(), self.msk.clone(), self.bs.clone())
+        self.reset()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(steps):
+                self.step(i, rows_mode=rows_mode, workspace=ws)
+        ms = []
+        for _ in range(2):
+            self.reset()
+            start = torch.cuda.Event(enable_timing=True)
+            stop = torch.cuda.Event(enable_timing=True)
+            start.record()
+            graph.replay()
+            stop.record()
+            torch.cuda.synchronize()
+            assert all(torch.equal(a, b) for a, b in zip((self.tok, self.msk, self.bs), want))
+            ms.append(start.elapsed_time(stop) / steps)
+        del graph
+        return ms[-1]
+
+
+def config_leg(name, args, dev, hip):
+    """Eager and graph-replayed step times of one workload, all rows and
+    active-block rows, with the LM head's fraction of the bf16 MFMA peak."""
+    import torch
+
+    from paper_2609_39859_amd import _binding, synth
+    cfg = synth.CONFIGS[name]
+    print("bench: workload %s B=%d L=%d d=%d V=%d" % (name, cfg.B, cfg.L, cfg.d, cfg.V),
+          file=sys.stderr, flush=True)
+    sb = StepBench(cfg, dev, hip)
+    flops = 2.0 * cfg.M * cfg.d * cfg.V
+    total, lm, _ = sb.timed(_binding.FORK_ROWS_ALL, args.steps, args.warmup)
+    ms = total / args.steps
+    lm_ms = sum(lm) / len(lm)
+    g_ms = sb.graph_timed(args.steps)
+    a_total, a_lm, _ = sb.timed(_binding.FORK_ROWS_ACTIVE, args.steps, args.warmup)
+    a_g_ms = sb.graph_timed(args.steps, _binding.FORK_ROWS_ACTIVE)
+    tf = flops / (lm_ms * 1e-3) / 1e12
+    out = {"workload": "B=%d, L=%d (prompt %d + gen %d), block_len %d, d=%d, V=%d, %s, tau=%g"
+                       % (cfg.B, cfg.L, cfg.P, cfg.G, cfg.block_len, cfg.d, cfg.V, cfg.dtype,
+                          cfg.tau),
+           "ms_per_step": ms, "steps_per_s": 1000.0 / ms, "positions_per_s": 1000.0 / ms * cfg.M,
+           "graph_ms_per_step": g_ms, "graph_steps_per_s": 1000.0 / g_ms,
+           "lmhead_ms": lm_ms,
+           "roofline": {"bound": "mfma", "achieved": tf, "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": tf / PEAK_BF16_TFLOPS,
+                        "kernel": "gemm_stats_bf16_kernel",
+                        "algorithmic_flops_per_launch": flops},
+           "step_mfma_frac_graph": flops / (g_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "step_ms_at_60pct_of_peak": flops / (0.6 * PEAK_BF16_TFLOPS * 1e12) * 1e3,
+           "active_rows_mode": {"ms_per_step": a_total / args.steps,
+                                "graph_ms_per_step": a_g_ms,
+                                "lmhead_ms": sum(a_lm) / len(a_lm)}}
+    del sb
+    torch.cuda.empty_cache()
     return out
 
 
@@ -282,6 +585,10 @@ def main():
                     help="skip the selection latency and bandwidth sweep")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measurement of the achievable MFMA and HBM rates")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the timings of the mid, rollout and long workloads")
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip the unfused torch step (context only)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device copy (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -316,64 +623,12 @@ def main():
         print("bench: ran 3 copies of 1 GiB (read 1 GiB + write 1 GiB each)",
               file=sys.stderr, flush=True)
 
-    W = synth.weights(cfg, device=dev)
-    n_batches = 4
-    hs = [synth.hidden(cfg, t, device=dev) for t in range(n_batches)]
-    tok0, msk0, bs0 = synth.initial_state(cfg)
-    tok, msk, bs = tok0.to(dev), msk0.to(dev), bs0.to(dev)
-    f32 = dict(dtype=torch.float32, device=dev)
-    conf, ent, logp = (torch.empty(M, **f32) for _ in range(3))
-    fb = torch.empty(B, dtype=torch.int32, device=dev)
-
     hip = _hip()
-
-    def reset():
-        # restart the decode so every timed step has masked positions to select
-        tok.copy_(tok0.to(dev))
-        msk.copy_(msk0.to(dev))
-        bs.copy_(bs0.to(dev))
-        torch.cuda.synchronize()
-
-    def timed(rows_mode, steps, warmup, temperature=0.0):
-        """Warm up, restart the decode, then time `steps` steps: total time
-        from torch events on the current stream, LM-head time per step from
-        HIP events the library records around that kernel on the same
-        stream."""
-        evs = []
-        for _ in range(2 * steps):
-            e = ctypes.c_void_p()
-            assert hip.hipEventCreate(ctypes.byref(e)) == 0
-            evs.append(e.value)
-
-        def step(i, events=None):
-            _binding.fork_step_ex(hs[i % n_batches], W, tok, msk, bs, BL, cfg.tau, conf, ent,
-                                  logp, fb, B=B, L=L, events=events, rows_mode=rows_mode,
-                                  temperature=temperature, seed=0x5EED, counter=i)
-
-        for i in range(warmup):
-            step(i)
-        torch.cuda.synchronize()
-        reset()
-        start = torch.cuda.Event(enable_timing=True)
-        stop = torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
-        start.record()
-        for i in range(steps):
-            step(i, (evs[2 * i], evs[2 * i + 1]))
-        stop.record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        lm = []
-        for i in range(steps):
-            ms = ctypes.c_float()
-            assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * i], evs[2 * i + 1]) == 0
-            lm.append(ms.value)
-        for e in evs:
-            hip.hipEventDestroy(e)
-        return start.elapsed_time(stop), lm, wall
+    sb = StepBench(cfg, dev, hip)
+    W, hs = sb.W, sb.hs
 
     print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
-    total_ms, lm_ms, wall = timed(_binding.FORK_ROWS_ALL, args.steps, args.warmup)
+    total_ms, lm_ms, wall = sb.timed(_binding.FORK_ROWS_ALL, args.steps, args.warmup)
 
     ms_per_step = total_ms / args.steps
     steps_per_s = 1000.0 / ms_per_step
@@ -409,14 +664,15 @@ def main():
                      "algorithmic_flops_per_launch": flops},
         "cpu_baseline": None,
     }
+    out["graph_ms_per_step"] = sb.graph_timed(args.steps)
     if not args.no_active_rows:
         # The same workload with the LM head restricted to each sequence's
         # active block (B*block_len rows): W is read once per step and the
         # per-row work is small, so this mode is bounded by HBM bandwidth.
         print("bench: timing %d steps, active-block rows only" % args.steps, file=sys.stderr,
               flush=True)
-        a_total, a_lm, _ = timed(_binding.FORK_ROWS_ACTIVE, args.steps, args.warmup)
-        reset()
+        a_total, a_lm, _ = sb.timed(_binding.FORK_ROWS_ACTIVE, args.steps, args.warmup)
+        sb.reset()
         Ma = B * BL
         a_ms = a_total / args.steps
         a_lm_ms = sum(a_lm) / len(a_lm)
@@ -425,6 +681,7 @@ def main():
         out["active_rows_mode"] = {
             "rows_per_step": Ma, "ms_per_step": a_ms, "steps_per_s": 1000.0 / a_ms,
             "lmhead_ms": a_lm_ms,
+            "graph_ms_per_step": sb.graph_timed(args.steps, _binding.FORK_ROWS_ACTIVE),
             "roofline": {"bound": "hbm", "achieved": a_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": a_gbs / PEAK_HBM_GBS,
                          "traffic": _traffic_per_launch("gemm_stats_bf16_rows_kernel"),
@@ -441,17 +698,27 @@ def main():
                                      "gemm_stats_bf16_rows_draw_kernel")):
             print("bench: timing %d steps, drawn candidates, %s" % (args.steps, label),
                   file=sys.stderr, flush=True)
-            d_total, d_lm, _ = timed(mode, args.steps, args.warmup, temperature=0.8)
-            reset()
+            d_total, d_lm, _ = sb.timed(mode, args.steps, args.warmup, temperature=0.8)
+            sb.reset()
             drawn[label] = {"ms_per_step": d_total / args.steps,
                             "steps_per_s": 1000.0 * args.steps / d_total,
                             "lmhead_ms": sum(d_lm) / len(d_lm), "kernel": kernel}
         out["drawn_candidates"] = drawn
     if not args.no_grpo:
         out["forkgrpo_likelihood"] = grpo_likelihood(args, hip, W, hs[0], dev)
+    if not args.no_context:
+        print("bench: unfused torch step (context)", file=sys.stderr, flush=True)
+        out["context_unfused_torch"] = context_unfused_torch(cfg, W, hs[0], sb.state0, dev,
+                                                             min(args.steps, 10))
+        torch.cuda.empty_cache()
     if not args.no_selection:
         print("bench: selection latency and bandwidth sweep", file=sys.stderr, flush=True)
         out["selection"] = selection(args, dev)
+        torch.cuda.empty_cache()
+    if not args.no_configs:
+        out["configs"] = {}
+        for name in ("mid", "rollout", "long"):
+            out["configs"][name] = config_leg(name, args, dev, hip)
     if not args.no_peaks:
         print("bench: measuring achievable MFMA and HBM rates", file=sys.stderr, flush=True)
         pk = measured_peaks(dev)
@@ -469,6 +736,8 @@ def main():
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)
+        print("bench: oracle CPU legs (tiny and mid whole steps)", file=sys.stderr, flush=True)
+        out["cpu_baseline"]["legs"] = cpu_legs()
     print(json.dumps(out), flush=True)
 
 
