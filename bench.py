@@ -306,12 +306,13 @@ def selection(args, dev):
                     bs=torch.zeros(B, dtype=torch.int32, device=dev),
                     fb=torch.empty(B, dtype=torch.int32, device=dev))
 
-    def run(B, L, BL, reps, warmup, nsets=1):
+    def run(B, L, BL, reps, warmup, nsets=1, layout=_binding.FORK_LAYOUT_ROW_MAJOR):
         sets = [make(B, L, B + L + k) for k in range(nsets)]
+        pm = layout == _binding.FORK_LAYOUT_POSITION_MAJOR
 
         def launch(x):
             _binding.select(x["conf"], x["am"], x["tok"], x["msk"], x["bs"], BL, 0.9, x["fb"],
-                            B=B, L=L)
+                            B=B, L=L, layout=layout)
         for k in range(warmup):
             launch(sets[k % nsets])
         torch.cuda.synchronize()
@@ -335,8 +336,9 @@ def selection(args, dev):
                    2 * (reps // nsets + (1 if k < reps % nsets else 0)) for k in range(nsets)]
         for x, n in zip(sets, per_set):
             assert int((x["fb"] == 1).sum().item()) == B
-            assert int(x["msk"].view(B, L)[:, :n].sum().item()) == 0
-            assert int(x["msk"].view(B, L)[:, n:].sum().item()) == B * (L - n)
+            m = x["msk"].view(L, B).t() if pm else x["msk"].view(B, L)
+            assert int(m[:, :n].sum().item()) == 0
+            assert int(m[:, n:].sum().item()) == B * (L - n)
         return start.elapsed_time(stop) * 1e3 / reps
 
     for name, B, L, BL in (("llada8b", 8, 512, 32), ("rollout", 64, 384, 32),
@@ -347,12 +349,14 @@ def selection(args, dev):
         nsets = max(1, -(-(512 << 20) // (set_bytes_per_seq * B)))
         reps = max(20, nsets)
         assert 3 + 2 * -(-reps // nsets) < 32   # each copy keeps masked positions
-        us = run(B, 32, 32, reps, 3, nsets)
-        gbs = SEL_BYTES_PER_SEQ * B / (us * 1e-6) / 1e9
-        out["sweep"].append({"B": B, "L": 32, "block_len": 32, "us": us, "GB_s": gbs,
-                             "frac_hbm": gbs / PEAK_HBM_GBS,
-                             "bytes_per_seq": SEL_BYTES_PER_SEQ, "batch_copies": nsets,
-                             "bytes_cycled": nsets * set_bytes_per_seq * B})
+        for layout, lname in ((_binding.FORK_LAYOUT_ROW_MAJOR, "row_major"),
+                              (_binding.FORK_LAYOUT_POSITION_MAJOR, "position_major")):
+            us = run(B, 32, 32, reps, 3, nsets, layout)
+            gbs = SEL_BYTES_PER_SEQ * B / (us * 1e-6) / 1e9
+            out["sweep"].append({"B": B, "L": 32, "block_len": 32, "layout": lname, "us": us,
+                                 "GB_s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+                                 "bytes_per_seq": SEL_BYTES_PER_SEQ, "batch_copies": nsets,
+                                 "bytes_cycled": nsets * set_bytes_per_seq * B})
     return out
 
 

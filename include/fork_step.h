@@ -230,14 +230,29 @@ int fork_step_noalloc(const fork_step_args* args);
    are invalid. */
 size_t fork_workspace_bytes(int32_t B, int32_t L, int32_t V);
 
+/* Layouts of the per-position arrays of fork_select (conf, entropy, argmax,
+   tokens, mask). */
+enum {
+  FORK_LAYOUT_ROW_MAJOR = 0,      /* position k of sequence b at b*L + k (as
+                                     everywhere else in this interface)       */
+  FORK_LAYOUT_POSITION_MAJOR = 1  /* position k of sequence b at k*B + b: the
+                                     sequences' entries for one position are
+                                     adjacent, so a batch whose sequences sit
+                                     at the same positions reads and commits
+                                     whole cache lines (large batches)        */
+};
+
 /* The unmasking rule alone (Algorithm 2; the `rule` variants of
    fork_step_args), applied in place to B sequences from per-position
    confidences and candidates computed elsewhere: exactly the selection stage
    of fork_step_ex, with the same arguments, semantics and outputs
    (out_fallback per sequence; out_ncommit and out_commit_pos optional).
    entropy ([B*L]) is needed by FORK_RULE_MAXENT, uniform ([B]) by
-   FORK_RULE_RANDOM.  B == 0 enqueues nothing (array pointers may be NULL).
-   Returns FORK_OK, FORK_EINVAL or FORK_EHIP. */
+   FORK_RULE_RANDOM.  `layout` (FORK_LAYOUT_*) orders conf, entropy, argmax,
+   tokens and mask; block_start, out_fallback, out_ncommit and
+   out_commit_pos ([B, block_len], row b for sequence b) do not depend on it,
+   and neither do the decisions.  B == 0 enqueues nothing (array pointers may
+   be NULL).  Returns FORK_OK, FORK_EINVAL or FORK_EHIP. */
 typedef struct fork_select_args {
   const float* conf;       /* [B*L] confidence of each position's candidate    */
   const float* entropy;    /* [B*L] or NULL                                    */
@@ -253,6 +268,7 @@ typedef struct fork_select_args {
   float tau;
   int32_t rule;
   void* stream;
+  int32_t layout;          /* FORK_LAYOUT_*                                    */
 } fork_select_args;
 int fork_select(const fork_select_args* args);
 

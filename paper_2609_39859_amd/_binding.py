@@ -31,6 +31,8 @@ FORK_RULE_RANDOM = 4
 FORK_ROWS_ALL = 0
 FORK_ROWS_ACTIVE = 1
 FORK_NOALLOC_SCRATCH_BYTES = 64 << 20
+FORK_LAYOUT_ROW_MAJOR = 0
+FORK_LAYOUT_POSITION_MAJOR = 1
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -81,7 +83,7 @@ class ForkSelectArgs(ctypes.Structure):
         ("tokens", _P), ("mask", _P), ("block_start", _P),
         ("out_fallback", _P), ("out_ncommit", _P), ("out_commit_pos", _P),
         ("B", _I32), ("L", _I32), ("block_len", _I32), ("tau", ctypes.c_float),
-        ("rule", _I32), ("stream", _P),
+        ("rule", _I32), ("stream", _P), ("layout", _I32),
     ]
 
 
@@ -350,8 +352,11 @@ def top_entropy(entropy: torch.Tensor, k: int, out_sel: torch.Tensor, stream=Non
 def select(conf: torch.Tensor, argmax: torch.Tensor, tokens: torch.Tensor, mask: torch.Tensor,
            block_start: torch.Tensor, block_len: int, tau: float, out_fallback: torch.Tensor, *,
            B: int, L: int, rule: int = FORK_RULE_LEFTMOST, entropy=None, uniform=None,
-           out_ncommit=None, out_commit_pos=None, stream=None) -> None:
-    """fork_select of the C ABI: the unmasking rule alone, in place."""
+           out_ncommit=None, out_commit_pos=None, stream=None,
+           layout: int = FORK_LAYOUT_ROW_MAJOR) -> None:
+    """fork_select of the C ABI: the unmasking rule alone, in place.  With
+    FORK_LAYOUT_POSITION_MAJOR the per-position tensors hold position k of
+    sequence b at k*B + b."""
     device = conf.device
     if device.type != "cuda":
         raise ValueError("fork_select runs on the GPU")
@@ -369,6 +374,7 @@ def select(conf: torch.Tensor, argmax: torch.Tensor, tokens: torch.Tensor, mask:
     a.out_commit_pos = _opt(out_commit_pos, "out_commit_pos", torch.int32, B * int(block_len),
                             device)
     a.B, a.L, a.block_len, a.tau, a.rule = B, L, int(block_len), float(tau), int(rule)
+    a.layout = int(layout)
     a.stream = _stream_handle(stream, device)
     _raise_on(lib().fork_select(ctypes.byref(a)))
 

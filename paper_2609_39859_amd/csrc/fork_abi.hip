@@ -24,7 +24,7 @@ static __device__ __align__(256) unsigned char scratch[FORK_NOALLOC_SCRATCH_BYTE
 
 namespace {
 
-constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
+constexpr int kVersion = 1 * 10000 + 1 * 100 + 0;
 constexpr size_t kAlign = 256;
 // Per-tile byte offsets of the LM-head kernel are 32-bit: 256 rows x d x 4 B
 // must stay below 2^31.
@@ -254,7 +254,7 @@ int enqueue_step(const fork_step_args* a, void* ws, const Layout& lay) {
   e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->out_conf,
                           a->out_entropy, a->fallback_uniform, argmax, a->tokens, a->mask,
                           a->block_start, a->out_fallback, a->out_ncommit, a->out_commit_pos,
-                          stream);
+                          /*position_major=*/false, stream);
   if (e != hipSuccess) return fail(FORK_EHIP, "select launch: %s", hipGetErrorString(e));
 
   static const bool sync_each = [] {
@@ -433,11 +433,14 @@ int fork_select(const fork_select_args* a) {
     return fail(FORK_EINVAL, "FORK_RULE_RANDOM needs uniform");
   if (a->rule == FORK_RULE_MAXENT && a->B > 0 && !a->entropy)
     return fail(FORK_EINVAL, "FORK_RULE_MAXENT needs entropy");
+  if (a->layout != FORK_LAYOUT_ROW_MAJOR && a->layout != FORK_LAYOUT_POSITION_MAJOR)
+    return fail(FORK_EINVAL, "unknown layout %d", a->layout);
   if (a->B == 0) return FORK_OK;  // an empty batch: nothing to enqueue
   hipError_t e = fork::launch_select(a->B, a->L, a->block_len, a->tau, a->rule, a->conf,
                                      a->entropy, a->uniform, a->argmax, a->tokens, a->mask,
                                      a->block_start, a->out_fallback, a->out_ncommit,
-                                     a->out_commit_pos, static_cast<hipStream_t>(a->stream));
+                                     a->out_commit_pos, a->layout == FORK_LAYOUT_POSITION_MAJOR,
+                                     static_cast<hipStream_t>(a->stream));
   if (e != hipSuccess) return fail(FORK_EHIP, "select launch: %s", hipGetErrorString(e));
   return FORK_OK;
 }

@@ -79,17 +79,21 @@ hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
 
 // Unmasking rule per sequence, in place.  ncommit / commit_pos may be null;
 // entropy is read by the highest-entropy rule, uniform by the random rule.
-// Batches of at least kLaneSelectMinB sequences with blocks of at most
-// kLaneSelectMaxBL positions run one lane per sequence, others one wave per
-// sequence; both give the same results.
+// Row-major state (element k of sequence b at b * L + k): batches of at
+// least kLaneSelectMinB sequences with blocks of at most kLaneSelectMaxBL
+// positions run one lane per sequence, others one wave per sequence.
+// Position-major state (at k * B + b): one lane per four sequences from
+// kPmWideMinB sequences on, one lane per sequence below.  All give the same
+// results.
 constexpr int kLaneSelectMinB = 4096;
 constexpr int kLaneSelectMaxBL = 64;
+constexpr int kPmWideMinB = 1 << 18;
 hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          const float* conf, const float* entropy, const float* uniform,
                          const int32_t* argmax,
                          int32_t* tokens, uint8_t* mask, int32_t* block_start,
                          int32_t* fallback, int32_t* ncommit,
-                         int32_t* commit_pos, hipStream_t stream);
+                         int32_t* commit_pos, bool position_major, hipStream_t stream);
 
 // ForkGRPO objective over n_groups groups of G rollouts (G <=
 // kMaxGroupSize); entries of rollout i are [offsets[i], offsets[i+1])

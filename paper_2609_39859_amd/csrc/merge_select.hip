@@ -307,6 +307,106 @@ __global__ __launch_bounds__(64) void select_kernel(
   }
 }
 
+// Element k of sequence b: row-major (b * L + k) or position-major
+// (k * B + b) state arrays.
+struct RowMajor {
+  int L;
+  __device__ size_t operator()(int b, int k) const { return (size_t)b * L + k; }
+};
+struct PosMajor {
+  int B;
+  __device__ size_t operator()(int b, int k) const { return (size_t)k * B + b; }
+};
+
+// The unmasking rule for sequence b by one lane, visiting the positions one
+// by one from block start s (already read from block_start[b]): skip
+// forward to the first block holding a masked position, then the threshold
+// set, the fallback pick and the commits.
+template <class At>
+__device__ void lane_rule(int b, int s, int L, int BL, float tau, int rule,
+                          const float* __restrict__ conf, const float* __restrict__ entropy,
+                          const float* __restrict__ uniform, const int32_t* __restrict__ argmax,
+                          int32_t* __restrict__ tokens, uint8_t* __restrict__ mask,
+                          int32_t* __restrict__ block_start, int32_t* __restrict__ fallback,
+                          int32_t* __restrict__ ncommit, int32_t* __restrict__ my_commits,
+                          At at) {
+  if (s < 0 || s > L) {
+    fallback[b] = -2;
+    if (ncommit) ncommit[b] = 0;
+    if (my_commits)
+      for (int i = 0; i < BL; ++i) my_commits[i] = -1;
+    return;
+  }
+  bool found = false;
+  while (s < L) {
+    const int e = min(s + BL, L);
+    for (int k = s; k < e && !found; ++k) found = mask[at(b, k)] != 0;
+    if (found) break;
+    s += BL;
+  }
+  if (!found) {
+    fallback[b] = -1;
+    if (ncommit) ncommit[b] = 0;
+    if (my_commits)
+      for (int i = 0; i < BL; ++i) my_commits[i] = -1;
+    return;
+  }
+  const int e = min(s + BL, L);
+  // threshold count, masked count, leftmost masked, extreme of the key
+  const float* key = rule == kMaxEnt ? entropy : conf;
+  const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
+  const bool lowest = rule == kMinConf;
+  int npass = 0, n = 0, first = -1, bi = -1;
+  float best = 0.f;
+  for (int k = s; k < e; ++k) {
+    const size_t idx = at(b, k);
+    if (!mask[idx]) continue;
+    ++n;
+    if (first < 0) first = k;
+    if (conf[idx] > tau) ++npass;
+    if (extreme) {
+      const float v = key[idx];
+      if (bi < 0 || (lowest ? v < best : v > best)) {
+        best = v;
+        bi = k;
+      }
+    }
+  }
+  const bool fb = npass == 0;
+  int pick = -1;
+  if (fb) {
+    if (rule == kLeftmost) {
+      pick = first;
+    } else if (rule == kRandom) {
+      int j = (int)(uniform[b] * (float)n);
+      j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
+      for (int k = s; k < e; ++k)
+        if (mask[at(b, k)] && j-- == 0) {
+          pick = k;
+          break;
+        }
+    } else {
+      pick = bi;
+    }
+  }
+  int written = 0;
+  for (int k = s; k < e; ++k) {
+    const size_t idx = at(b, k);
+    if (!mask[idx]) continue;
+    if (fb ? (k == pick) : (conf[idx] > tau)) {
+      tokens[idx] = argmax[idx];
+      mask[idx] = 0;
+      if (my_commits) my_commits[written] = k;
+      ++written;
+    }
+  }
+  if (my_commits)
+    for (int i = written; i < BL; ++i) my_commits[i] = -1;
+  fallback[b] = fb ? 1 : 0;
+  block_start[b] = s;
+  if (ncommit) ncommit[b] = written;
+}
+
 // The same rule with one lane per sequence, for large batches of short
 // blocks: each lane walks its block position by position, so a wave keeps
 // the loads of 64 sequences in flight instead of one (the wave-per-sequence
@@ -402,73 +502,149 @@ __global__ __launch_bounds__(256) void select_lanes_kernel(
     }
     s += BL;  // nothing masked there: continue the skip-forward below
   }
-  // skip forward to the first block holding a masked position
-  bool found = false;
-  while (s < L) {
-    const int e = min(s + BL, L);
-    for (int k = s; k < e && !found; ++k) found = mask[base + k] != 0;
-    if (found) break;
-    s += BL;
+  lane_rule(b, s, L, BL, tau, rule, conf, entropy, uniform, argmax, tokens, mask, block_start,
+            fallback, ncommit, my_commits, RowMajor{L});
+}
+
+// Position-major state (element (b, k) at k * B + b): one lane per group of
+// kS consecutive sequences (kS = 4 for large batches, 1 otherwise, so that
+// small batches still spread over many waves).  When the group shares its
+// block start and the block has at most 32 positions, each position of the
+// block comes in as one load of the group's kS confidences (and keys) and
+// one of its kS mask bytes, so a wave's loads cover whole cache lines; the
+// loads are issued kChunk positions at a time before any is used, and the
+// rule is decided on 32-bit masks in registers.  Sequences outside that case
+// take the position-by-position path.  Decisions are those of the row-major
+// kernels.
+template <int kS> struct PmVec;
+template <> struct PmVec<1> {
+  typedef float F;
+  typedef uint8_t M;
+  static __device__ float get(F v, int) { return v; }
+};
+template <> struct PmVec<4> {
+  typedef float4 F;
+  typedef uint32_t M;
+  static __device__ float get(F v, int j) {
+    return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
   }
-  if (!found) {
-    fallback[b] = -1;
-    if (ncommit) ncommit[b] = 0;
-    if (my_commits)
-      for (int i = 0; i < BL; ++i) my_commits[i] = -1;
+};
+
+template <int kS, int kChunk>
+__global__ __launch_bounds__(256) void select_pm_kernel(
+    int B, int L, int BL, float tau, int rule, const float* __restrict__ conf,
+    const float* __restrict__ entropy, const float* __restrict__ uniform,
+    const int32_t* __restrict__ argmax, int32_t* __restrict__ tokens,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ block_start,
+    int32_t* __restrict__ fallback, int32_t* __restrict__ ncommit,
+    int32_t* __restrict__ commit_pos) {
+  typedef typename PmVec<kS>::F VF;
+  typedef typename PmVec<kS>::M VM;
+  const int b0 = kS * (blockIdx.x * 256 + threadIdx.x);
+  if (b0 >= B) return;
+  const PosMajor at{B};
+  const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
+  const float* key = rule == kMaxEnt ? entropy : conf;
+  bool wide = b0 + kS <= B && (B % kS) == 0 && BL <= 32 &&
+              ((reinterpret_cast<uintptr_t>(conf) | reinterpret_cast<uintptr_t>(key)) &
+               (sizeof(VF) - 1)) == 0 &&
+              (reinterpret_cast<uintptr_t>(mask) & (sizeof(VM) - 1)) == 0;
+  int s = 0;
+  if (wide) {
+    s = block_start[b0];
+    for (int j = 1; j < kS; ++j) wide = wide && block_start[b0 + j] == s;
+    wide = wide && s >= 0 && s + BL <= L;
+  }
+  if (!wide) {
+    for (int b = b0; b < min(b0 + kS, B); ++b)
+      lane_rule(b, block_start[b], L, BL, tau, rule, conf, entropy, uniform, argmax, tokens,
+                mask, block_start, fallback, ncommit,
+                commit_pos ? commit_pos + (size_t)b * BL : nullptr, at);
     return;
   }
-  const int e = min(s + BL, L);
-  // threshold count, masked count, leftmost masked, extreme of the key
-  const float* key = rule == kMaxEnt ? entropy : conf;
-  const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
+  uint32_t mb[kS], pb[kS];
+  float best[kS];
+  int bi[kS];
+#pragma unroll
+  for (int j = 0; j < kS; ++j) {
+    mb[j] = pb[j] = 0;
+    best[j] = 0.f;
+    bi[j] = -1;
+  }
   const bool lowest = rule == kMinConf;
-  int npass = 0, n = 0, first = -1, bi = -1;
-  float best = 0.f;
-  for (int k = s; k < e; ++k) {
-    if (!mask[base + k]) continue;
-    ++n;
-    if (first < 0) first = k;
-    if (conf[base + k] > tau) ++npass;
-    if (extreme) {
-      const float v = key[base + k];
-      if (bi < 0 || (lowest ? v < best : v > best)) {
-        best = v;
-        bi = k;
+  for (int i0 = 0; i0 < BL; i0 += kChunk) {
+    VM mv[kChunk];
+    VF cv[kChunk], kv[kChunk];
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      if (i0 + u < BL) {
+        const size_t row = (size_t)(s + i0 + u) * B + b0;
+        mv[u] = *reinterpret_cast<const VM*>(mask + row);
+        cv[u] = *reinterpret_cast<const VF*>(conf + row);
+        if (extreme) kv[u] = *reinterpret_cast<const VF*>(key + row);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const int i = i0 + u;
+      if (i >= BL) break;
+#pragma unroll
+      for (int j = 0; j < kS; ++j) {
+        const bool m = (((uint32_t)mv[u] >> (8 * j)) & 0xffu) != 0;
+        const float c = PmVec<kS>::get(cv[u], j);
+        const float k = extreme ? PmVec<kS>::get(kv[u], j) : c;
+        mb[j] |= (uint32_t)m << i;
+        pb[j] |= (uint32_t)(m && c > tau) << i;
+        // branch-free: a select per value (lowest position on equal keys)
+        const bool better = lowest ? k < best[j] : k > best[j];
+        const bool take = extreme && m && (bi[j] < 0 || better);
+        best[j] = take ? k : best[j];
+        bi[j] = take ? i : bi[j];
       }
     }
   }
-  const bool fb = npass == 0;
-  int pick = -1;
-  if (fb) {
-    if (rule == kLeftmost) {
-      pick = first;
-    } else if (rule == kRandom) {
-      int j = (int)(uniform[b] * (float)n);
-      j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
-      for (int k = s; k < e; ++k)
-        if (mask[base + k] && j-- == 0) {
-          pick = k;
-          break;
-        }
-    } else {
-      pick = bi;
+#pragma unroll
+  for (int j = 0; j < kS; ++j) {
+    const int b = b0 + j;
+    int32_t* my_commits = commit_pos ? commit_pos + (size_t)b * BL : nullptr;
+    if (mb[j] == 0) {  // nothing masked in the block at s: skip forward
+      lane_rule(b, s, L, BL, tau, rule, conf, entropy, uniform, argmax, tokens, mask,
+                block_start, fallback, ncommit, my_commits, at);
+      continue;
     }
-  }
-  int written = 0;
-  for (int k = s; k < e; ++k) {
-    if (!mask[base + k]) continue;
-    if (fb ? (k == pick) : (conf[base + k] > tau)) {
-      tokens[base + k] = argmax[base + k];
-      mask[base + k] = 0;
+    const bool fb = pb[j] == 0;
+    uint32_t commit = pb[j];
+    if (fb) {
+      int pick;
+      if (rule == kLeftmost) {
+        pick = __ffs(mb[j]) - 1;
+      } else if (rule == kRandom) {
+        const int n = __popc(mb[j]);
+        int r = (int)(uniform[b] * (float)n);
+        r = r > n - 1 ? n - 1 : (r < 0 ? 0 : r);
+        uint32_t rest = mb[j];
+        for (int t = 0; t < r; ++t) rest &= rest - 1;  // drop the r lowest
+        pick = __ffs(rest) - 1;
+      } else {
+        pick = bi[j];
+      }
+      commit = 1u << pick;
+    }
+    int written = 0;
+    for (uint32_t rest = commit; rest; rest &= rest - 1) {
+      const int k = s + __ffs(rest) - 1;
+      const size_t idx = at(b, k);
+      tokens[idx] = argmax[idx];
+      mask[idx] = 0;
       if (my_commits) my_commits[written] = k;
       ++written;
     }
+    if (my_commits)
+      for (int i = written; i < BL; ++i) my_commits[i] = -1;
+    fallback[b] = fb ? 1 : 0;
+    block_start[b] = s;
+    if (ncommit) ncommit[b] = written;
   }
-  if (my_commits)
-    for (int i = written; i < BL; ++i) my_commits[i] = -1;
-  fallback[b] = fb ? 1 : 0;
-  block_start[b] = s;
-  if (ncommit) ncommit[b] = written;
 }
 
 // Active block of each sequence (first block from block_start holding a
@@ -533,8 +709,16 @@ hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          const float* conf, const float* entropy, const float* uniform,
                          const int32_t* argmax, int32_t* tokens, uint8_t* mask,
                          int32_t* block_start, int32_t* fallback, int32_t* ncommit,
-                         int32_t* commit_pos, hipStream_t stream) {
-  if (B >= kLaneSelectMinB && block_len <= kLaneSelectMaxBL)
+                         int32_t* commit_pos, bool position_major, hipStream_t stream) {
+  if (position_major && B >= kPmWideMinB)
+    hipLaunchKernelGGL((select_pm_kernel<4, 8>), dim3((unsigned)(((B + 3) / 4 + 255) / 256)),
+                       dim3(256), 0, stream, B, L, block_len, tau, rule, conf, entropy, uniform,
+                       argmax, tokens, mask, block_start, fallback, ncommit, commit_pos);
+  else if (position_major)
+    hipLaunchKernelGGL((select_pm_kernel<1, 32>), dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
+                       stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
+                       tokens, mask, block_start, fallback, ncommit, commit_pos);
+  else if (B >= kLaneSelectMinB && block_len <= kLaneSelectMaxBL)
     hipLaunchKernelGGL(select_lanes_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
                        stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
                        tokens, mask, block_start, fallback, ncommit, commit_pos);

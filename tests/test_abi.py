@@ -40,7 +40,7 @@ def test_exports_are_c_symbols():
 
 def test_version_and_workspace_sizes():
     L = _binding.lib()
-    assert L.fork_version() == 10000
+    assert L.fork_version() == 10100
     # per-tile partials (16 B per position per 256-entry vocabulary tile,
     # padded to 256 B) + candidates and active-row list (4 B per position each)
     # + the per-tile drawn candidates (as large as the partials)
@@ -232,6 +232,7 @@ def _sel_args(**kw):
 
 
 @pytest.mark.parametrize("kw", [
+    dict(layout=2), dict(layout=-1),
     dict(conf=0), dict(argmax=0), dict(tokens=0), dict(mask=0), dict(block_start=0),
     dict(out_fallback=0), dict(B=-1), dict(L=-1), dict(block_len=0), dict(block_len=9),
     dict(tau=float("nan")), dict(rule=5), dict(rule=4), dict(rule=3),

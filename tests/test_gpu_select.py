@@ -35,17 +35,35 @@ def _state(B, L, V, seed):
     return conf, ent, am, tok, msk, bs, uni
 
 
-def _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule):
+def _pm(x, B, L):
+    """Row-major [B*L] -> position-major [L*B] (position k of sequence b at
+    k*B + b)."""
+    return np.ascontiguousarray(np.asarray(x).reshape(B, L).T).reshape(-1)
+
+
+def _rm(x, B, L):
+    return np.ascontiguousarray(np.asarray(x).reshape(L, B).T).reshape(-1)
+
+
+def _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule,
+         layout=_binding.FORK_LAYOUT_ROW_MAJOR):
+    """fork_select on row-major host state; with the position-major layout
+    the per-position arrays are transposed for the call and back after it,
+    so the results compare directly."""
     t = lambda x: torch.as_tensor(np.ascontiguousarray(x), device=DEV)
-    tok_d, msk_d, bs_d = t(tok.copy()), t(msk.copy()), t(bs.copy())
+    pm = layout == _binding.FORK_LAYOUT_POSITION_MAJOR
+    lay = (lambda x: _pm(x, B, L)) if pm else (lambda x: x)
+    tok_d, msk_d, bs_d = t(lay(tok).copy()), t(lay(msk).copy()), t(bs.copy())
     fb = torch.full((B,), -9, dtype=torch.int32, device=DEV)
     nc = torch.full((B,), -9, dtype=torch.int32, device=DEV)
     cp = torch.full((B * BL,), -9, dtype=torch.int32, device=DEV)
-    _binding.select(t(conf), t(am), tok_d, msk_d, bs_d, BL, tau, fb, B=B, L=L, rule=rule,
-                    entropy=t(ent), uniform=t(uni), out_ncommit=nc, out_commit_pos=cp)
+    _binding.select(t(lay(conf)), t(lay(am)), tok_d, msk_d, bs_d, BL, tau, fb, B=B, L=L,
+                    rule=rule, entropy=t(lay(ent)), uniform=t(uni), out_ncommit=nc,
+                    out_commit_pos=cp, layout=layout)
     torch.cuda.synchronize()
-    return (tok_d.cpu().numpy(), msk_d.cpu().numpy(), bs_d.cpu().numpy(), fb.cpu().numpy(),
-            nc.cpu().numpy(), cp.cpu().numpy().reshape(B, BL))
+    back = (lambda x: _rm(x, B, L)) if pm else (lambda x: x)
+    return (back(tok_d.cpu().numpy()), back(msk_d.cpu().numpy()), bs_d.cpu().numpy(),
+            fb.cpu().numpy(), nc.cpu().numpy(), cp.cpu().numpy().reshape(B, BL))
 
 
 SHAPES = [
@@ -57,13 +75,36 @@ SHAPES = [
 ]
 
 
+PM_SHAPES = [
+    # position-major: B % 4 == 0 with shared block starts takes the wide path
+    (5, 61, 7), (6, 33, 32), (4096, 32, 32), (4096, 64, 16), (4100, 40, 8), (4099, 33, 32),
+    (8, 100, 65), (4097, 1, 1), (1024, 48, 33),
+]
+
+
 @pytest.mark.parametrize("B,L,BL", SHAPES)
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
 def test_select_matches_oracle(B, L, BL, rule):
+    _check_against_oracle(B, L, BL, rule, _binding.FORK_LAYOUT_ROW_MAJOR)
+
+
+@pytest.mark.parametrize("B,L,BL", PM_SHAPES)
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("shared_start", [False, True])
+def test_select_position_major_matches_oracle(B, L, BL, rule, shared_start):
+    """The position-major layout against the oracle (on the transposed
+    state), with random block starts and with every sequence at the same
+    block start (the wide path)."""
+    _check_against_oracle(B, L, BL, rule, _binding.FORK_LAYOUT_POSITION_MAJOR, shared_start)
+
+
+def _check_against_oracle(B, L, BL, rule, layout, shared_start=False):
     _need_gpu()
     conf, ent, am, tok, msk, bs, uni = _state(B, L, 1000, B * 31 + L + BL + rule)
+    if shared_start:
+        bs[:] = min(L - BL, 3)
     for tau in (0.3, 0.9):
-        g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule)
+        g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule, layout)
         o = oracle.select_ex(conf, am, tok, msk, bs, B, L, BL, float(np.float32(tau)), rule,
                              entropy=ent, uniform=uni)
         for k, (x, y) in enumerate(zip(g[:5], o)):
@@ -103,3 +144,47 @@ def test_bad_block_start_reported_in_data_on_both_paths(B):
     g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.5, 0)
     assert g[3][:3].tolist() == [-2, -2, -1]
     assert np.all(g[1][:3 * L] == 1) and np.all(g[4][:3] == 0) and np.all(g[5][:3] == -1)
+
+
+@pytest.mark.parametrize("B", [1 << 16, 1 << 18])
+def test_position_major_sweep_shape_matches_row_major(B):
+    """The benchmark's sweep shape (blocks of 32 positions, one block per
+    sequence, every sequence falling back), 2^16 sequences (one per lane)
+    and 2^18 (four per lane): position-major and row-major give the same
+    decisions, and every sequence commits its leftmost masked position."""
+    _need_gpu()
+    L, BL = 32, 32
+    rng = np.random.default_rng(11)
+    conf = (rng.random(B * L) * 0.03).astype(np.float32)
+    am = rng.integers(0, 126464, B * L).astype(np.int32)
+    tok = np.full(B * L, -1, np.int32)
+    msk = np.ones(B * L, np.uint8)
+    msk.reshape(B, L)[:, :5] = 0
+    bs = np.zeros(B, np.int32)
+    ent = np.zeros(B * L, np.float32)
+    uni = np.zeros(B, np.float32)
+    a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.9, 0)
+    b = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.9, 0,
+             _binding.FORK_LAYOUT_POSITION_MAJOR)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    assert np.all(a[3] == 1) and np.all(a[5][:, 0] == 5) and np.all(a[5][:, 1:] == -1)
+    assert np.array_equal(a[0].reshape(B, L)[:, 5], am.reshape(B, L)[:, 5])
+
+
+@pytest.mark.parametrize("B,L,BL", [((1 << 18), 40, 32), ((1 << 18) + 2, 33, 16),
+                                    ((1 << 18), 20, 20)])
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
+def test_position_major_large_batches_match_row_major(B, L, BL, rule):
+    """Batches large enough for four sequences per lane (and one not a
+    multiple of four): random states, half of them sharing a block start,
+    position-major against row-major (itself checked against the oracle)."""
+    _need_gpu()
+    conf, ent, am, tok, msk, bs, uni = _state(B, L, 1000, B + L + BL + rule)
+    bs[: B // 2] = min(L - BL, 2)
+    for tau in (0.3, 0.9):
+        a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule)
+        b = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule,
+                 _binding.FORK_LAYOUT_POSITION_MAJOR)
+        for k, (x, y) in enumerate(zip(a, b)):
+            assert np.array_equal(x, y), k
