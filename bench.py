@@ -246,6 +246,9 @@ def measured_peaks(dev):
     lib.fork_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     lib.fork_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                     ctypes.c_int, ctypes.c_void_p]
+    lib.fork_probe_mfma_data.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                         ctypes.c_void_p]
     stream = torch.cuda.current_stream(dev).cuda_stream
     blocks, iters = 7904, 256      # the LM head's grid and K/16 at the LLaDA-8B shape
     out = torch.empty(blocks * 512, device=dev)
@@ -258,6 +261,24 @@ def measured_peaks(dev):
     stop.record()
     torch.cuda.synchronize()
     mfma = blocks * 8.0 * iters * 8 * 32768 / (start.elapsed_time(stop) * 1e-3) / 1e12
+    # the same flops on operands drawn like the LM head's data: W_head
+    # N(0, 1/d) and hidden rows N(0, 1) x RMS U[0.5, 2] (d = 4096), bf16
+    nfrag = 1024
+    gen = torch.Generator(device=dev).manual_seed(0xF00D)
+    a_src = (torch.randn(nfrag * 12 * 64 * 8, generator=gen, device=dev) / 64.0).to(torch.bfloat16)
+    b_src = (torch.randn(nfrag * 12 * 64 * 8, generator=gen, device=dev) *
+             (0.5 + 1.5 * torch.rand(nfrag * 12 * 64 * 8, generator=gen, device=dev))
+             ).to(torch.bfloat16)
+    assert lib.fork_probe_mfma_data(blocks, 100, a_src.data_ptr(), b_src.data_ptr(), nfrag,
+                                    out.data_ptr(), stream) == 0
+    torch.cuda.synchronize()
+    start.record()
+    assert lib.fork_probe_mfma_data(blocks, iters, a_src.data_ptr(), b_src.data_ptr(), nfrag,
+                                    out.data_ptr(), stream) == 0
+    stop.record()
+    torch.cuda.synchronize()
+    mfma_data = blocks * 8.0 * iters * 8 * 32768 / (start.elapsed_time(stop) * 1e-3) / 1e12
+    del a_src, b_src
     n = (1 << 30) // 16
     src = torch.ones(n * 16, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
@@ -272,11 +293,14 @@ def measured_peaks(dev):
     assert bool(dst[-1] == 1)
     hbm = 2.0 * (1 << 30) * reps / (start.elapsed_time(stop) * 1e-3) / 1e9
     del src, dst
-    return {"mfma_bf16_TFLOP_s": mfma, "hbm_copy_GB_s": hbm,
+    return {"mfma_bf16_TFLOP_s": mfma_data, "mfma_bf16_TFLOP_s_constant_operands": mfma,
+            "hbm_copy_GB_s": hbm,
             "how": "MFMA: 7904 workgroups x 8 waves x 256 rounds of 8 independent "
                    "v_mfma_f32_32x32x16_bf16 on register operands (the flops of one LM-head "
-                   "launch); HBM: streaming copy of 1 GiB (4 x 16 B per thread per "
-                   "iteration), read + write counted, 5 repetitions"}
+                   "launch), operands alternating between two sets of fragments loaded from "
+                   "random bf16 data drawn like W_head and the hidden rows (the rate quoted), "
+                   "and on one constant set (constant_operands); HBM: streaming copy of 1 GiB "
+                   "(4 x 16 B per thread per iteration), read + write counted, 5 repetitions"}
 
 
 def selection(args, dev):

@@ -39,6 +39,57 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* __rest
   out[blockIdx.x * 512 + threadIdx.x] = s;
 }
 
+// The same MFMA stream on operands with the statistics of the LM head's
+// real data: each wave holds two sets of fragments loaded from `a_src` /
+// `b_src` (random bf16 values drawn like W_head and the hidden rows), four
+// A and two B fragments per set as one 16-element step of the LM-head
+// kernel uses, and alternates between the sets every round, so consecutive
+// MFMAs see changing operand bits as in the LM head.
+__global__ __launch_bounds__(512) void mfma_data_kernel(int iters, const bf16x8* __restrict__ a_src,
+                                                        const bf16x8* __restrict__ b_src, int nfrag,
+                                                        float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int wave = (blockIdx.x * 8 + (threadIdx.x >> 6)) % nfrag;
+  bf16x8 a0[4], b0[2], a1[4], b1[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a0[i] = a_src[((size_t)wave * 12 + i) * 64 + lane];
+    a1[i] = a_src[((size_t)wave * 12 + 4 + i) * 64 + lane];
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    b0[j] = b_src[((size_t)wave * 12 + 8 + j) * 64 + lane];
+    b1[j] = b_src[((size_t)wave * 12 + 10 + j) * 64 + lane];
+  }
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  for (int it = 0; it < iters; it += 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s += acc[i][j][e];
+  out[blockIdx.x * 512 + threadIdx.x] = s;
+}
+
 // Streaming copy: each thread moves four 16-byte elements per iteration
 // (consecutive threads on consecutive elements), grid-stride.
 __global__ __launch_bounds__(256) void stream_copy_kernel(const uint4* __restrict__ src,
@@ -65,6 +116,18 @@ extern "C" {
 int fork_probe_mfma(int blocks, int iters, float* out, void* stream) {
   hipLaunchKernelGGL(mfma_peak_kernel, dim3((unsigned)blocks), dim3(512), 0,
                      static_cast<hipStream_t>(stream), iters, out);
+  return (int)hipGetLastError();
+}
+
+// Launches the MFMA probe on data operands: a_src and b_src hold nfrag x 12
+// x 64 fragments of 8 bf16 (wave w of the grid uses set w % nfrag); iters
+// even.  Same flop count as fork_probe_mfma.  Returns a hipError_t.
+int fork_probe_mfma_data(int blocks, int iters, const void* a_src, const void* b_src, int nfrag,
+                         float* out, void* stream) {
+  hipLaunchKernelGGL(mfma_data_kernel, dim3((unsigned)blocks), dim3(512), 0,
+                     static_cast<hipStream_t>(stream), iters,
+                     static_cast<const bf16x8*>(a_src), static_cast<const bf16x8*>(b_src), nfrag,
+                     out);
   return (int)hipGetLastError();
 }
 

@@ -838,3 +838,45 @@ def test_gpu_resume_matches_uninterrupted():
         for u, v in zip(final, ref_final):
             assert np.array_equal(u, v)
     _say("resume: %d-step decode reproduced after stops at %s" % (T, [1, T // 2, T - 1]))
+
+
+@pytest.mark.parametrize("B,L,d,V,dtype,BL", RAGGED + [(8, 512, 64, 3000, torch.bfloat16, 32),
+                                                       (3, 200, 64, 700, torch.bfloat16, 64)])
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("rows_mode", [0, 1])
+def test_step_decisions_equal_standalone_selection(B, L, d, V, dtype, BL, rule, rows_mode):
+    """The step's own selection decides exactly what fork_select decides on
+    the step's confidences, candidates and entropies from the same state,
+    for every rule and both row modes, with a drawn-candidate case."""
+    _need_gpu()
+    gen = torch.Generator().manual_seed(11 * B + L + d + V + rule)
+    M = B * L
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(dtype).to(DEV)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(dtype).to(DEV)
+    rng = np.random.default_rng(M + V + 5 + rule)
+    msk = (rng.random(M) < 0.5).astype(np.uint8)
+    tok = np.where(msk, -1, rng.integers(0, V, M)).astype(np.int32)
+    bs = rng.integers(0, L + 1, B).astype(np.int32)
+    if B > 1:
+        msk[(B - 1) * L:] = 0  # an idle sequence
+    uni = rng.random(B).astype(np.float32)
+    for tau, temperature in ((0.05, 0.0), (0.3, 0.0), (0.2, 0.9)):
+        g = gpu_step(h, W, tok, msk, bs, B, L, BL, tau, rule=rule, uniform=uni,
+                     rows_mode=rows_mode, temperature=temperature, seed=SEED, counter=3)
+        t = lambda x: torch.as_tensor(np.ascontiguousarray(x)).to(DEV)
+        conf = np.nan_to_num(g.conf, nan=0.0)
+        ent = np.nan_to_num(g.entropy, nan=0.0)
+        am = np.where(g.argmax == -7, 0, g.argmax).astype(np.int32)
+        tok_d, msk_d, bs_d = t(tok.copy()), t(msk.copy()), t(bs.copy())
+        fb = torch.full((B,), -9, dtype=torch.int32, device=DEV)
+        nc = torch.full((B,), -9, dtype=torch.int32, device=DEV)
+        cp = torch.full((B * BL,), -9, dtype=torch.int32, device=DEV)
+        _binding.select(t(conf), t(am), tok_d, msk_d, bs_d, BL, tau, fb, B=B, L=L, rule=rule,
+                        entropy=t(ent), uniform=t(uni), out_ncommit=nc, out_commit_pos=cp)
+        torch.cuda.synchronize()
+        assert np.array_equal(g.tokens, tok_d.cpu().numpy())
+        assert np.array_equal(g.mask, msk_d.cpu().numpy())
+        assert np.array_equal(g.block_start, bs_d.cpu().numpy())
+        assert np.array_equal(g.fallback, fb.cpu().numpy())
+        assert np.array_equal(g.ncommit, nc.cpu().numpy())
+        assert np.array_equal(g.commit_pos, cp.cpu().numpy().reshape(B, BL))
