@@ -692,6 +692,16 @@ def main():
                      "algorithmic_flops_per_launch": flops},
         "cpu_baseline": None,
     }
+    pk = None
+    if not args.no_peaks:
+        # right after the headline timing, so that the probes run in the same
+        # thermal state as the timed LM-head launches
+        print("bench: measuring achievable MFMA and HBM rates", file=sys.stderr, flush=True)
+        pk = measured_peaks(dev)
+        out["measured_peaks"] = pk
+        rf = out["roofline"]
+        rf["measured_peak"] = pk["mfma_bf16_TFLOP_s"]
+        rf["frac_of_measured_peak"] = rf["achieved"] / pk["mfma_bf16_TFLOP_s"]
     out["graph_ms_per_step"] = sb.graph_timed(args.steps)
     if not args.no_active_rows:
         # The same workload with the LM head restricted to each sequence's
@@ -717,6 +727,10 @@ def main():
                          "algorithmic_bytes_per_launch": a_bytes,
                          "mfma_frac": 2.0 * Ma * d * V / (a_lm_ms * 1e-3) / 1e12
                                       / PEAK_BF16_TFLOPS}}
+        if pk:
+            ar = out["active_rows_mode"]["roofline"]
+            ar["measured_peak"] = pk["hbm_copy_GB_s"]
+            ar["frac_of_measured_peak"] = ar["achieved"] / pk["hbm_copy_GB_s"]
     if not args.no_drawn:
         # Candidates drawn at sampling temperature 0.8 (Gumbel-max over
         # Philox4x32-10 draws for the active blocks' positions).
@@ -743,24 +757,13 @@ def main():
         print("bench: selection latency and bandwidth sweep", file=sys.stderr, flush=True)
         out["selection"] = selection(args, dev)
         torch.cuda.empty_cache()
+        if pk:
+            for x in out["selection"]["sweep"]:
+                x["frac_of_measured_hbm"] = x["GB_s"] / pk["hbm_copy_GB_s"]
     if not args.no_configs:
         out["configs"] = {}
         for name in ("mid", "rollout", "long"):
             out["configs"][name] = config_leg(name, args, dev, hip)
-    if not args.no_peaks:
-        print("bench: measuring achievable MFMA and HBM rates", file=sys.stderr, flush=True)
-        pk = measured_peaks(dev)
-        out["measured_peaks"] = pk
-        rf = out["roofline"]
-        rf["measured_peak"] = pk["mfma_bf16_TFLOP_s"]
-        rf["frac_of_measured_peak"] = rf["achieved"] / pk["mfma_bf16_TFLOP_s"]
-        if "active_rows_mode" in out:
-            ar = out["active_rows_mode"]["roofline"]
-            ar["measured_peak"] = pk["hbm_copy_GB_s"]
-            ar["frac_of_measured_peak"] = ar["achieved"] / pk["hbm_copy_GB_s"]
-        if "selection" in out:
-            for x in out["selection"]["sweep"]:
-                x["frac_of_measured_hbm"] = x["GB_s"] / pk["hbm_copy_GB_s"]
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)
