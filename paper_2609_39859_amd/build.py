@@ -38,10 +38,32 @@ def compile_flags():
 
 
 def build(verbose: bool = False) -> str:
-    """Compile and link libforkstep.so and libforkprobe.so; returns the
-    path of libforkstep.so."""
+    """Compile and link libforkstep.so and libforkprobe.so, then the plain-C
+    example that drives one step through the C ABI; returns the path of
+    libforkstep.so."""
     _build_lib(PROBE_LIB, PROBE_SOURCES, verbose)
-    return _build_lib(LIB, SOURCES, verbose)
+    lib = _build_lib(LIB, SOURCES, verbose)
+    build_c_example(verbose)
+    return lib
+
+
+C_EXAMPLE_SRC = os.path.join(ROOT, "tests", "native", "abi_c_step.c")
+C_EXAMPLE = os.path.join(HERE, "_build", "abi_c_step")
+
+
+def build_c_example(verbose: bool = False) -> str:
+    """gcc -std=c99 build of tests/native/abi_c_step.c against the public
+    header, libforkstep.so and the HIP runtime's C API."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    os.makedirs(os.path.dirname(C_EXAMPLE), exist_ok=True)
+    cmd = ["gcc", "-std=c99", "-O1", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(rocm, "include"), "-I", INCLUDE, C_EXAMPLE_SRC,
+           "-L", HERE, "-lforkstep", "-L", os.path.join(rocm, "lib"), "-lamdhip64", "-lm",
+           "-Wl,-rpath,$ORIGIN/..", "-o", C_EXAMPLE]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return C_EXAMPLE
 
 
 def _build_lib(lib_path: str, sources, verbose: bool) -> str:

@@ -315,3 +315,23 @@ def test_noalloc_empty_batch_is_a_no_op():
     nulls = dict(hidden=0, W_head=0, tokens=0, mask=0, block_start=0, out_conf=0,
                  out_entropy=0, out_logp=0, out_fallback=0, B=0)
     assert L.fork_step_noalloc(ctypes.byref(_args(**nulls))) == _binding.FORK_OK
+
+
+def test_plain_c_caller(tmp_path):
+    """tests/native/abi_c_caller.c: the public header compiles as C99
+    (-pedantic), the library links from C, and host-side validation answers
+    through fork_step_ex / fork_last_error without a GPU."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no host C compiler")
+    exe = str(tmp_path / "abi_c_caller")
+    lib_dir = os.path.dirname(_binding.LIB_PATH)
+    subprocess.run([gcc, "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror",
+                    "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "native", "abi_c_caller.c"), "-L", lib_dir,
+                    "-lforkstep", "-Wl,-rpath," + lib_dir, "-o", exe], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True)
+    assert r.returncode == 0, (r.returncode, r.stderr)
+    assert "c abi ok" in r.stdout

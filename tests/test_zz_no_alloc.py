@@ -131,3 +131,43 @@ def test_noalloc_rejects_what_does_not_fit():
     a.workspace_bytes = 1 << 20
     import ctypes
     assert _binding.lib().fork_step_noalloc(ctypes.byref(a)) == _binding.FORK_EINVAL
+
+
+def test_noalloc_under_graph_capture():
+    """The callers it is for: a step captured into a HIP graph (after a first
+    call on the device has looked up the scratch address).  Every replay,
+    with eager state resets and synchronisations between them, gives the
+    eager fork_step_ex result bit for bit."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(DEV)
+    cfg = synth.CONFIGS["mid"]
+    W, h, tok0, msk0, bs0 = _inputs(cfg, 2)
+    ref = _run(_with_workspace(cfg), cfg, W, h, tok0, msk0, bs0)
+    _run(_binding.fork_step_noalloc, cfg, W, h, tok0, msk0, bs0)  # first call on the device
+    M, B, BL = cfg.M, cfg.B, cfg.block_len
+    tok, msk, bs = tok0.clone(), msk0.clone(), bs0.clone()
+    f32 = dict(dtype=torch.float32, device=DEV)
+    i32 = dict(dtype=torch.int32, device=DEV)
+    conf, ent, logp, lse = (torch.empty(M, **f32) for _ in range(4))
+    am = torch.empty(M, **i32)
+    fb, nc = torch.empty(B, **i32), torch.empty(B, **i32)
+    cp = torch.empty(B * BL, **i32)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        _binding.fork_step_noalloc(h, W, tok, msk, bs, BL, cfg.tau, conf, ent, logp, fb, B=B,
+                                   L=cfg.L, out_lse=lse, out_argmax=am, out_ncommit=nc,
+                                   out_commit_pos=cp)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        tok.copy_(tok0)
+        msk.copy_(msk0)
+        bs.copy_(bs0)
+        for t in (conf, ent, logp, lse):
+            t.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = dict(conf=conf, entropy=ent, logp=logp, lse=lse, argmax=am, fallback=fb,
+                   ncommit=nc, commit_pos=cp, tokens=tok, mask=msk, block_start=bs)
+        _same(got, ref, "graph replay %d" % rep)
