@@ -880,3 +880,61 @@ def test_step_decisions_equal_standalone_selection(B, L, d, V, dtype, BL, rule, 
         assert np.array_equal(g.fallback, fb.cpu().numpy())
         assert np.array_equal(g.ncommit, nc.cpu().numpy())
         assert np.array_equal(g.commit_pos, cp.cpu().numpy().reshape(B, BL))
+
+
+@pytest.mark.parametrize("name", ["rollout", "long"])
+def test_full_size_active_rows_decode(name):
+    """A whole full-size decode with the LM head on the active blocks' rows
+    only (FORK_ROWS_ACTIVE): AR-order fallback commits across every block
+    boundary, rows outside the active blocks never written, and at the
+    boundary steps the committed rows plus sampled active rows against the
+    oracle."""
+    _need_gpu()
+    cfg = synth.CONFIGS[name]
+    W = synth.weights(cfg, device=DEV)
+    Wb = None
+    tok, msk, bs = (x.to(DEV) for x in synth.initial_state(cfg))
+    B, L, BL, M, P = cfg.B, cfg.L, cfg.block_len, cfg.M, cfg.P
+    f32 = dict(dtype=torch.float32, device=DEV)
+    conf, ent, logp, lse = (torch.full((M,), float("nan"), **f32) for _ in range(4))
+    am = torch.full((M,), -7, dtype=torch.int32, device=DEV)
+    fb = torch.empty(B, dtype=torch.int32, device=DEV)
+    cp = torch.empty(B * BL, dtype=torch.int32, device=DEV)
+    checks = _decode_checks(cfg)
+    rng = np.random.default_rng(cfg.seed + 98)
+    rep = Report()
+    written = np.zeros(M, bool)
+    _say("full-size active-rows decode %s: %d steps" % (name, cfg.G))
+    for t in range(cfg.G):
+        h = synth.hidden(cfg, t, device=DEV)
+        bs_before = bs.cpu().numpy() if t in checks else None
+        msk_before = msk.cpu().numpy() if t in checks else None
+        _binding.fork_step_ex(h, W, tok, msk, bs, BL, cfg.tau, conf, ent, logp, fb, B=B, L=L,
+                              out_lse=lse, out_argmax=am, out_commit_pos=cp,
+                              rows_mode=_binding.FORK_ROWS_ACTIVE)
+        fbh = fb.cpu().numpy()
+        cph = cp.cpu().numpy().reshape(B, BL)
+        assert np.all(fbh == 1), "step %d: fallback %s" % (t, fbh)
+        assert np.all(cph[:, 0] == P + t) and np.all(cph[:, 1:] == -1), "step %d: commits" % t
+        if t not in checks:
+            continue
+        if Wb is None:
+            Wb = host_bits(W)
+        active = _active_rows(cfg, msk_before, bs_before)
+        g = types.SimpleNamespace(conf=conf.cpu().numpy(), entropy=ent.cpu().numpy(),
+                                  logp=logp.cpu().numpy(), lse=lse.cpu().numpy(),
+                                  argmax=am.cpu().numpy())
+        written |= ~np.isnan(g.conf)
+        committed = np.arange(B) * L + P + t
+        rows = np.union1d(committed, rng.choice(active, 16, replace=False))
+        _say("active-rows decode %s step %d: oracle on %d rows" % (name, t, rows.size))
+        ref = oracle.row_stats(host_bits(h), Wb, rows)
+        compare_stats(g, ref, rows, host_bits(h), Wb, cfg.d, rep)
+        assert np.array_equal(tok.cpu().numpy()[committed], g.argmax[committed])
+    # only rows of some step's active block were ever written (the blocks of
+    # the generation region); the prompt never
+    assert not written.reshape(B, L)[:, :P].any()
+    assert not msk.cpu().numpy().reshape(B, L)[:, P:].any()
+    _say("full-size active-rows decode %s: %d rows checked (%d near-tie), max err %s" % (
+        name, rep.rows, rep.near_tie_rows, {k: "%.2e" % v for k, v in rep.max_err.items()}))
+    record(rep, name, steps=cfg.G, decode=True, rows_mode=1, tau=cfg.tau)
