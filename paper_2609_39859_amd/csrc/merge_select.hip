@@ -92,7 +92,15 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
       const float4 p2 = col[(size_t)(j + 128) * M], p3 = col[(size_t)(j + 192) * M];
       acc = merge2(merge2(merge2(merge2(acc, p0), p1), p2), p3);
     }
-    for (; j < nvt; j += 64) acc = merge2(acc, col[(size_t)j * M]);
+    // the last (at most three) tiles of the stream: loads issued together,
+    // merged in the same increasing order
+    float4 q[3];
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      if (j + 64 * t < nvt) q[t] = col[(size_t)(j + 64 * t) * M];
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      if (j + 64 * t < nvt) acc = merge2(acc, q[t]);
   }
   // streams 4w + {0..3} of this position: lanes pl, pl + 16, pl + 32, pl + 48
 #pragma unroll
@@ -104,8 +112,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   const bool drawn = sample_row && live && sample_row[r] >= 0;
   float4 sacc = make_float4(-INFINITY, __int_as_float(0x7fffffff), 0.f, 0.f);
   if (drawn) {
+    // the winner does not depend on the order: loads eight at a time
     const float4* scol = spartials + r;
-    for (int k = c; k < nvt; k += 64) sacc = pick_drawn(sacc, scol[(size_t)k * M]);
+    for (int k0 = c; k0 < nvt; k0 += 512) {
+      float4 q[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (k0 + 64 * t < nvt) q[t] = scol[(size_t)(k0 + 64 * t) * M];
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (k0 + 64 * t < nvt) sacc = pick_drawn(sacc, q[t]);
+    }
   }
   if (sample_row) {
 #pragma unroll
