@@ -197,6 +197,85 @@ __global__ __launch_bounds__(64) void select_kernel(
   const size_t base = (size_t)b * L;
   int32_t* my_commits = commit_pos ? commit_pos + (size_t)b * BL : nullptr;
 
+  if (BL <= 64) {
+    // lane i <-> position s + i of a block: the block's mask byte,
+    // confidence, candidate (and entropy) arrive together, and the rule is
+    // decided from registers
+    int s = block_start[b];
+    int status = (s < 0 || s > L) ? -2 : -1;
+    bool masked = false;
+    float cf = 0.f;
+    int cand = 0;
+    unsigned long long mball = 0;
+    while (status == -1 && s < L) {
+      const int k = s + lane;
+      const bool in = k < min(s + BL, L);
+      const uint8_t m = in ? mask[base + k] : 0;
+      cf = in ? conf[base + k] : 0.f;
+      cand = in ? argmax[base + k] : 0;
+      masked = m != 0;
+      mball = ballot(masked);
+      if (mball) status = 0;
+      else s += BL;
+    }
+    if (status != 0) {
+      if (lane == 0) {
+        fallback[b] = status;
+        if (ncommit) ncommit[b] = 0;
+      }
+      if (my_commits && lane < BL) my_commits[lane] = -1;
+      return;
+    }
+    const int k = s + lane;
+    const bool pass = masked && cf > tau;
+    const unsigned long long pball = ballot(pass);
+    const bool fb = pball == 0;
+    int pick = -1;
+    if (fb) {
+      if (rule == kLeftmost) {
+        pick = s + __ffsll((long long)mball) - 1;
+      } else if (rule == kRandom) {
+        const int n = __popcll(mball);
+        int j = (int)(uniform[b] * (float)n);
+        j = j > n - 1 ? n - 1 : (j < 0 ? 0 : j);
+        const int below = __popcll(mball & ((1ull << lane) - 1ull));
+        pick = s + __ffsll((long long)ballot(masked && below == j)) - 1;
+      } else {
+        // extreme of confidence (highest or lowest) or of entropy (highest),
+        // lowest position on ties
+        const bool lowest = rule == kMinConf;
+        float best = masked ? (rule == kMaxEnt ? entropy[base + k] : cf) : 0.f;
+        int bi = masked ? k : 0x7fffffff;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          const float ob = __shfl_xor(best, off);
+          const int oi = __shfl_xor(bi, off);
+          const bool better = lowest ? ob < best : ob > best;
+          const bool take =
+              oi != 0x7fffffff && (bi == 0x7fffffff || better || (ob == best && oi < bi));
+          best = take ? ob : best;
+          bi = take ? oi : bi;
+        }
+        pick = bi;
+      }
+    }
+    const bool commit = masked && (fb ? k == pick : pass);
+    const unsigned long long cball = ballot(commit);
+    if (commit) {
+      tokens[base + k] = cand;
+      mask[base + k] = 0;
+      if (my_commits) my_commits[__popcll(cball & ((1ull << lane) - 1ull))] = k;
+    }
+    const int written = __popcll(cball);
+    if (my_commits && lane >= written && lane < BL) my_commits[lane] = -1;
+    if (lane == 0) {
+      fallback[b] = fb ? 1 : 0;
+      block_start[b] = s;
+      if (ncommit) ncommit[b] = written;
+    }
+    return;
+  }
+
   int s = block_start[b];
   int status = 0;
   if (s < 0 || s > L) {
