@@ -807,11 +807,11 @@ hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          int32_t* block_start, int32_t* fallback, int32_t* ncommit,
                          int32_t* commit_pos, bool position_major, hipStream_t stream) {
   if (position_major && B >= kPmWideMinB)
-    hipLaunchKernelGGL((select_pm_kernel<4, 8>), dim3((unsigned)(((B + 3) / 4 + 255) / 256)),
+    hipLaunchKernelGGL((select_pm_kernel<4, 4>), dim3((unsigned)(((B + 3) / 4 + 255) / 256)),
                        dim3(256), 0, stream, B, L, block_len, tau, rule, conf, entropy, uniform,
                        argmax, tokens, mask, block_start, fallback, ncommit, commit_pos);
   else if (position_major)
-    hipLaunchKernelGGL((select_pm_kernel<1, 32>), dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
+    hipLaunchKernelGGL((select_pm_kernel<1, 16>), dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
                        stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
                        tokens, mask, block_start, fallback, ncommit, commit_pos);
   else if (B >= kLaneSelectMinB && block_len <= kLaneSelectMaxBL)
