@@ -13,13 +13,15 @@
 //
 // Work decomposition (gfx950 / CDNA4), common to both element types:
 //   * one workgroup = 256 vocabulary rows x 256 positions, 8 wave64s laid out
-//     2 (vocabulary) x 4 (positions); each wave owns 128 x 64 outputs as
-//     4 x 2 tiles of 32x32 MFMA accumulators (fp32);
+//     2 (vocabulary) x 4 (positions); each wave owns 128 x 64 outputs (fp32
+//     accumulators): 8 x 4 blocks of 16 x 16 (v_mfma_f32_16x16x32_bf16) on
+//     the bf16 path, 4 x 2 blocks of 32 x 32 (v_mfma_f32_32x32x2f32) on the
+//     fp32 path;
 //   * the MFMA "A" operand is W (vocabulary on the MFMA M axis) and "B" is
-//     hidden, so each lane's accumulators hold 16 vocabulary values of ONE
-//     position: the vocabulary reduction is mostly in-lane, plus one
-//     exchange with lane^32 and one LDS exchange between the two vocabulary
-//     waves;
+//     hidden, so each lane's accumulators hold vocabulary values of whole
+//     positions: the vocabulary reduction is mostly in-lane (32 or 64 values
+//     per position), plus shuffles between the lanes holding the same
+//     position and one LDS exchange between the two vocabulary waves;
 //   * K is staged through LDS in 128-byte slabs per row (whole cache lines),
 //     the 16-byte chunk c of row r stored at chunk slot c ^ f(r) with
 //     f(r) = (r & 7) ^ ((r >> 3) & 1): the fragment reads of 16 consecutive
@@ -33,10 +35,13 @@
 // directly (no register staging).  W gets a 3-slot ring (prefetched two
 // stages ahead: it streams from HBM), hidden a 2-slot ring (one stage ahead:
 // it stays in the last-level cache): 5 x 32 KiB = the whole 160 KiB of LDS.
-// One barrier per 64-element K stage; inside a stage the fragment reads of
-// the next 16-element sub-step are interleaved with the current MFMAs, and
-// the buffer loads of later stages are spread over the stage in small groups
-// so that no wave stalls its MFMA stream behind a burst of loads.
+// One barrier per 64-element K stage, placed after the first MFMAs of the
+// stage's second 32-element step so that queued MFMAs cover it; the fragment
+// reads of the next step are interleaved with the current MFMAs, and the
+// buffer loads of later stages are spread over the stage one at a time so
+// that no wave stalls its MFMA stream behind a burst of loads.  The 16x16x32
+// MFMA shape moves the same bytes per flop as 32x32x16 and, on this GPU,
+// sustains a higher clock under the same power limit.
 // fp32 path (small problems): register-staged double buffer.
 //
 // Drawn candidates (sampling temperature tau > 0, Section 2): for the
@@ -49,11 +54,14 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace fork {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 512;
 constexpr int kSlab = 128;                   // bytes of K per row per stage
@@ -137,110 +145,151 @@ __device__ __forceinline__ float gumbel_key(float z, float inv_tau, uint32_t w) 
   return fmaf(z, inv_tau, -__builtin_amdgcn_logf(e) * kLn2);
 }
 
-// Vocabulary index held by accumulator element `e` of MFMA tile `i` in this
-// lane (32x32 output layout: column = lane % 32, row = 8*(e/4) + 4*(lane/32)
-// + e%4), relative to the wave's first vocabulary row.
-__device__ __forceinline__ int acc_row(int i, int e, int lane) {
-  return i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-}
+// Accumulator layouts.  In both, a lane's accumulators hold vocabulary values
+// (MFMA rows) of whole positions (MFMA columns), so the reduction over the
+// vocabulary is mostly in-lane.
+//
+// Acc16 (bf16 path, v_mfma_f32_16x16x32_bf16): a wave's 128 x 64 outputs are
+// 8 x 4 blocks of 16 x 16; element e of block (i, j) in lane l is row
+// 16 i + 4 (l / 16) + e, column 16 j + l % 16.  The four lanes l % 16 + 16 g
+// (g = 0..3) hold the 128 rows of a column, 32 each.
+struct Acc16 {
+  typedef f32x4 Arr[8][4];
+  static constexpr int kNI = 8, kNJ = 4, kNE = 4;
+  static constexpr int kLeaders = 16;  // lanes 0..15 hold one copy of each column
+  __device__ static float get(const Arr& a, int i, int j, int e) { return a[i][j][e]; }
+  __device__ static void set(Arr& a, int i, int j, int e, float v) { a[i][j][e] = v; }
+  __device__ static int row(int i, int e, int lane) { return i * 16 + (lane >> 4) * 4 + e; }
+  __device__ static int col(int j, int lane) { return j * 16 + (lane & 15); }
+  // combine the copies of a column: lanes 16 and 32 apart
+  template <class F>
+  __device__ static void across(F&& f) {
+    f(16);
+    f(32);
+  }
+};
 
-// Per-(position, tile) statistics from the accumulators of one wave, combined
-// across the two vocabulary waves through LDS, stored to partials.
+// Acc32 (fp32 path, v_mfma_f32_32x32x2f32): 4 x 2 blocks of 32 x 32; element
+// e of block (i, j) in lane l is row 32 i + 8 (e / 4) + 4 (l / 32) + e % 4,
+// column 32 j + l % 32.  Lanes l and l ^ 32 hold the 128 rows of a column.
+struct Acc32 {
+  typedef f32x16 Arr[4][2];
+  static constexpr int kNI = 4, kNJ = 2, kNE = 16;
+  static constexpr int kLeaders = 32;
+  __device__ static float get(const Arr& a, int i, int j, int e) { return a[i][j][e]; }
+  __device__ static void set(Arr& a, int i, int j, int e, float v) { a[i][j][e] = v; }
+  __device__ static int row(int i, int e, int lane) {
+    return i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+  }
+  __device__ static int col(int j, int lane) { return j * 32 + (lane & 31); }
+  template <class F>
+  __device__ static void across(F&& f) {
+    f(32);
+  }
+};
+
 // What the epilogue produces besides the per-tile statistics.
 enum EpilogueMode { kGreedy = 0, kDrawn = 1, kTarget = 2 };
 
-// Drawn candidates (kDrawn) go through a second LDS exchange and a second
-// partials array (see SampleArgs); the logit of a given token (kTarget) is
-// stored by the one lane that holds it.
-// Statistics of the 64 logits one lane holds for column j (rows vbase +
-// acc_row(i, e, lane), increasing in (i, e)), combined with the lane 32
-// apart that holds the other 64 rows of the column: the maximum m, the
-// lowest row holding it, s = sum e^(z-m) and t = sum e^(z-m)(z-m).
-// Branch-free.  Unless kFull (every row < V), rows past V are set to -inf in
-// acc first, so that no pass needs a row test.
-template <bool kFull>
-__device__ __forceinline__ void column_stats(f32x16 (&acc)[4][2], int j, int lane, int vbase,
+// Statistics of the logits of column j that this lane holds (rows vbase +
+// Lay::row(i, e, lane), increasing in (i, e)), combined with the lanes that
+// hold the column's other rows: the maximum m, the lowest row holding it,
+// s = sum e^(z-m) and t = sum e^(z-m)(z-m).  Branch-free.  Unless kFull
+// (every row < V), rows past V are set to -inf in acc first, so that no pass
+// needs a row test.
+template <class Lay, bool kFull>
+__device__ __forceinline__ void column_stats(typename Lay::Arr& acc, int j, int lane, int vbase,
                                              int V, float& m_out, int& idx_out, float& s_out,
                                              float& t_out) {
   if (!kFull) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < Lay::kNI; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if (vbase + acc_row(i, e, lane) >= V) acc[i][j][e] = -INFINITY;
+      for (int e = 0; e < Lay::kNE; ++e)
+        if (vbase + Lay::row(i, e, lane) >= V) Lay::set(acc, i, j, e, -INFINITY);
   }
   float m = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < Lay::kNI; ++i)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) m = fmaxf(m, acc[i][j][e]);
+    for (int e = 0; e < Lay::kNE; ++e) m = fmaxf(m, Lay::get(acc, i, j, e));
   // the lowest row holding m: scan from the highest row down
   int idx = 0x7fffffff;
 #pragma unroll
-  for (int i = 3; i >= 0; --i)
+  for (int i = Lay::kNI - 1; i >= 0; --i)
 #pragma unroll
-    for (int e = 15; e >= 0; --e) idx = acc[i][j][e] == m ? vbase + acc_row(i, e, lane) : idx;
-  {
-    const float mo = __shfl_xor(m, 32);
-    const int io = __shfl_xor(idx, 32);
+    for (int e = Lay::kNE - 1; e >= 0; --e)
+      idx = Lay::get(acc, i, j, e) == m ? vbase + Lay::row(i, e, lane) : idx;
+  Lay::across([&](int off) {
+    const float mo = __shfl_xor(m, off);
+    const int io = __shfl_xor(idx, off);
     const bool take = mo > m || (mo == m && io < idx);
     m = take ? mo : m;
     idx = take ? io : idx;
-  }
+  });
   float s = 0.f, tl = 0.f;
   if (m > -INFINITY) {
     const float nml = -m * kLog2e;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < Lay::kNI; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < Lay::kNE; ++e) {
         // (z - m) * log2(e) with one rounding; the moment is summed in
         // these units and scaled by ln 2 once
-        const float dl = fmaf(acc[i][j][e], kLog2e, nml);
+        const float dl = fmaf(Lay::get(acc, i, j, e), kLog2e, nml);
         const float ex = __builtin_amdgcn_exp2f(dl);
         s += ex;
         // a -inf row has ex = 0: keep 0 * -inf out of the moment
         tl = fmaf(ex, kFull ? dl : fmaxf(dl, -1e30f), tl);
       }
   }
-  s += __shfl_xor(s, 32);
-  tl += __shfl_xor(tl, 32);
+  // lanes holding the same column add in the same order: identical results
+  Lay::across([&](int off) {
+    s += __shfl_xor(s, off);
+    tl += __shfl_xor(tl, off);
+  });
   m_out = m;
   idx_out = idx;
   s_out = s;
   t_out = tl * kLn2;
 }
 
-// kFull: the tile's 256 vocabulary rows are all < V (every tile but a
-// ragged last one), so no row test is compiled in.
-template <int kMode, bool kFull>
-__device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char* smem, int tid,
-                                              int lane, int wv, int wp, int vt, int v0, int p0,
-                                              int M, int V, float4* __restrict__ partials,
-                                              const SampleArgs& sa, const TargetArgs& ta) {
+// Per-(position, tile) statistics from the accumulators of one wave, combined
+// across the two vocabulary waves through LDS, stored to partials.  Drawn
+// candidates (kDrawn) go through a second LDS exchange and a second partials
+// array (see SampleArgs); the logit of a given token (kTarget) is stored by
+// the one lane that holds it.  kFull: the tile's 256 vocabulary rows are all
+// < V (every tile but a ragged last one), so no row test is compiled in.
+template <class Lay, int kMode, bool kFull>
+__device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned char* smem,
+                                              int tid, int lane, int wv, int wp, int vt, int v0,
+                                              int p0, int M, int V,
+                                              float4* __restrict__ partials, const SampleArgs& sa,
+                                              const TargetArgs& ta) {
   constexpr bool kDraw = kMode == kDrawn;
   constexpr bool full = kFull;
   float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
   float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
   const int vbase = v0 + wv * 128;
+  const bool leader = lane < Lay::kLeaders;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < Lay::kNJ; ++j) {
     float m, s, t;
     int idx;
-    column_stats<kFull>(acc, j, lane, vbase, V, m, idx, s, t);
-    const int col = wp * 64 + j * 32 + (lane & 31);
-    if (lane < 32) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
+    column_stats<Lay, kFull>(acc, j, lane, vbase, V, m, idx, s, t);
+    const int col = wp * 64 + Lay::col(j, lane);
+    if (leader) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
     if (kMode == kTarget) {
       const int tk = p0 + col < M ? ta.token[p0 + col] : -1;
       if (tk >= vbase && tk < vbase + 128 && tk < V) {
         float zt = 0.f;
         bool hit = false;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < Lay::kNI; ++i)
 #pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (vbase + acc_row(i, e, lane) == tk) {
-              zt = acc[i][j][e];
+          for (int e = 0; e < Lay::kNE; ++e)
+            if (vbase + Lay::row(i, e, lane) == tk) {
+              zt = Lay::get(acc, i, j, e);
               hit = true;
             }
         if (hit) ta.z[p0 + col] = zt;
@@ -252,11 +301,13 @@ __device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char
         float best = -INFINITY, bz = 0.f;
         int bidx = 0x7fffffff;
         if (srow >= 0) {
+          // elements 4g .. 4g + 3 of a block are four consecutive rows from
+          // a multiple of 4: one generator call yields their four words
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < Lay::kNI; ++i)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const int vq = vbase + acc_row(i, 4 * g, lane);  // multiple of 4
+            for (int g = 0; g < Lay::kNE / 4; ++g) {
+              const int vq = vbase + Lay::row(i, 4 * g, lane);
               if (full || vq < V) {
                 const uint4 w = philox4x32_10(make_uint4((uint32_t)vq >> 2, (uint32_t)srow,
                                                          sa.counter, 0u),
@@ -264,7 +315,7 @@ __device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char
                 const uint32_t words[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                  const float z = acc[i][j][4 * g + c];
+                  const float z = Lay::get(acc, i, j, 4 * g + c);
                   const float key = gumbel_key(z, sa.inv_tau, words[c]);
                   if ((full || vq + c < V) && key > best) {
                     best = key;
@@ -275,14 +326,16 @@ __device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char
               }
             }
         }
-        const float ob = __shfl_xor(best, 32), oz = __shfl_xor(bz, 32);
-        const int oi = __shfl_xor(bidx, 32);
-        if (ob > best || (ob == best && oi < bidx)) {
-          best = ob;
-          bidx = oi;
-          bz = oz;
-        }
-        if (lane < 32) sred[wv * kTileP + col] = make_float4(best, __int_as_float(bidx), bz, 0.f);
+        Lay::across([&](int off) {
+          const float ob = __shfl_xor(best, off), oz = __shfl_xor(bz, off);
+          const int oi = __shfl_xor(bidx, off);
+          if (ob > best || (ob == best && oi < bidx)) {
+            best = ob;
+            bidx = oi;
+            bz = oz;
+          }
+        });
+        if (leader) sred[wv * kTileP + col] = make_float4(best, __int_as_float(bidx), bz, 0.f);
       }
     }
   }
@@ -301,15 +354,17 @@ __device__ __forceinline__ void epilogue_tile(f32x16 (&acc)[4][2], unsigned char
   }
 }
 
-template <int kMode>
-__device__ __forceinline__ void epilogue(f32x16 (&acc)[4][2], unsigned char* smem, int tid,
+template <class Lay, int kMode>
+__device__ __forceinline__ void epilogue(typename Lay::Arr& acc, unsigned char* smem, int tid,
                                          int lane, int wv, int wp, int vt, int v0, int p0, int M,
                                          int V, float4* __restrict__ partials,
                                          const SampleArgs& sa, const TargetArgs& ta) {
   if (v0 + kTileV <= V)
-    epilogue_tile<kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+    epilogue_tile<Lay, kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa,
+                                    ta);
   else
-    epilogue_tile<kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+    epilogue_tile<Lay, kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials,
+                                     sa, ta);
 }
 
 __device__ __forceinline__ void barrier_nofence() {
@@ -396,140 +451,157 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     const int c = (q & 1) ? dchunk1 : dchunk0;
     return (s * 8 + c < kchunks) ? base[q] + (unsigned)(s * kSlab) : kOutOfRange;
   };
-  auto issue_W2 = [&](int s, int slot, int q0) {  // sub-blocks q0, q0 + 1 of W stage s
-#pragma unroll
-    for (int q = q0; q < q0 + 2; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsW, (__attribute__((address_space(3))) void*)(smem + slot * kOperandBytes + (wave * 4 + q) * 1024),
-          16, src_off(qoff, s, q), 0, 0, 0);
+  auto issue_W1 = [&](int s, int slot, int q) {  // sub-block q of W stage s
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rsW, (__attribute__((address_space(3))) void*)(smem + slot * kOperandBytes + (wave * 4 + q) * 1024),
+        16, src_off(qoff, s, q), 0, 0, 0);
+  };
+  auto issue_H1 = [&](int s, int slot, int q) {  // sub-block q of hidden stage s
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rsH, (__attribute__((address_space(3))) void*)(smem + (3 + slot) * kOperandBytes + (wave * 4 + q) * 1024),
+        16, src_off(hoff, s, q), 0, 0, 0);
   };
   auto issue_W = [&](int s, int slot) {
-    issue_W2(s, slot, 0);
-    issue_W2(s, slot, 2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) issue_W1(s, slot, q);
   };
   auto issue_H = [&](int s, int slot) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsH, (__attribute__((address_space(3))) void*)(smem + (3 + slot) * kOperandBytes + (wave * 4 + q) * 1024),
-          16, src_off(hoff, s, q), 0, 0, 0);
+    for (int q = 0; q < 4; ++q) issue_H1(s, slot, q);
   };
 
-  f32x16 acc[4][2];
+  Acc16::Arr acc;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
 
-  // Fragment addressing: rows arow + 32i share the swizzle of arow.
-  const int arow = wv * 128 + (lane & 31);
-  const int brow = wp * 64 + (lane & 31);
-  const int khalf = lane >> 5;  // lanes 32..63 supply the upper 8 of 16 K values
+  // Fragments of one 32-element K step: A fragment i = W rows arow + 16 i,
+  // B fragment j = positions brow + 16 j; lane group kq = lane / 16 supplies
+  // 16-byte chunk kq of the step (the same chunk of both operands, so each
+  // MFMA sums over the step's 32 K values).  Rows 16 apart share a swizzle.
+  const int arow = wv * 128 + (lane & 15);
+  const int brow = wp * 64 + (lane & 15);
+  const int kq = lane >> 4;
   const int fa = swz(arow), fb = swz(brow);
-
-  auto load_frags = [&](int ws, int hs, int kk, bf16x8 (&a)[4], bf16x8 (&b)[2]) {
-    const unsigned char* sa = smem + ws * kOperandBytes;
-    const unsigned char* sb = smem + (3 + hs) * kOperandBytes;
-    const int chunk = kk * 2 + khalf;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = *reinterpret_cast<const bf16x8*>(sa + (arow + i * 32) * kSlab + ((chunk ^ fa) << 4));
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      b[j] = *reinterpret_cast<const bf16x8*>(sb + (brow + j * 32) * kSlab + ((chunk ^ fb) << 4));
+  auto rd_a = [&](int ws, int kk, int i) {
+    const int chunk = kk * 4 + kq;
+    return *reinterpret_cast<const bf16x8*>(smem + ws * kOperandBytes + (arow + 16 * i) * kSlab +
+                                            ((chunk ^ fa) << 4));
   };
-  // Eight MFMAs on (ac, bc) with the six reads of the next fragments (an, bn)
-  // interleaved one per MFMA.  `mode` adds loads after the sixth MFMA:
-  // 1 = hidden stage s_dma (4 loads), 2 / 3 = W stage s_dma sub-blocks 0-1 /
-  // 2-3 (2 loads), each pair separated by an MFMA.
-  auto phase = [&](const bf16x8 (&ac)[4], const bf16x8 (&bc)[2], int ws, int hs, int kk,
-                   bf16x8 (&an)[4], bf16x8 (&bn)[2], int mode, int s_dma, int slot_dma) {
-    const unsigned char* sa = smem + ws * kOperandBytes;
-    const unsigned char* sb = smem + (3 + hs) * kOperandBytes;
-    const int chunk = kk * 2 + khalf;
-    const int ca = (chunk ^ fa) << 4, cb = (chunk ^ fb) << 4;
-    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[0], bc[0], acc[0][0], 0, 0, 0);
-    bn[0] = *reinterpret_cast<const bf16x8*>(sb + brow * kSlab + cb);
-    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[0], bc[1], acc[0][1], 0, 0, 0);
-    bn[1] = *reinterpret_cast<const bf16x8*>(sb + (brow + 32) * kSlab + cb);
-    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[1], bc[0], acc[1][0], 0, 0, 0);
-    an[0] = *reinterpret_cast<const bf16x8*>(sa + arow * kSlab + ca);
-    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[1], bc[1], acc[1][1], 0, 0, 0);
-    an[1] = *reinterpret_cast<const bf16x8*>(sa + (arow + 32) * kSlab + ca);
-    acc[2][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[0], acc[2][0], 0, 0, 0);
-    an[2] = *reinterpret_cast<const bf16x8*>(sa + (arow + 64) * kSlab + ca);
-    acc[2][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[2], bc[1], acc[2][1], 0, 0, 0);
-    an[3] = *reinterpret_cast<const bf16x8*>(sa + (arow + 96) * kSlab + ca);
-    if (mode == 1) issue_H(s_dma, slot_dma);
-    else if (mode == 2) issue_W2(s_dma, slot_dma, 0);
-    else if (mode == 3) issue_W2(s_dma, slot_dma, 2);
-    acc[3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[0], acc[3][0], 0, 0, 0);
-    acc[3][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[3], bc[1], acc[3][1], 0, 0, 0);
-#pragma unroll
-    for (int q = 0; q < 6; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-    }
-    if (mode == 1) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // buffer loads
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    } else if (mode >= 2) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    } else {
+  auto rd_b = [&](int hs, int kk, int j) {
+    const int chunk = kk * 4 + kq;
+    return *reinterpret_cast<const bf16x8*>(smem + (3 + hs) * kOperandBytes +
+                                            (brow + 16 * j) * kSlab + ((chunk ^ fb) << 4));
+  };
+  // One K step: 32 MFMAs on (a, bc), block row i at a time.  After the four
+  // MFMAs of row i, a[i] is refilled with the fragment of step kkn (slots
+  // wsn / hsn), and the four bn are read in between.  `dma` spreads four
+  // buffer loads over the rows: 1 = W stage s_dma (rows 0..3), 2 = hidden
+  // stage s_dma (rows 1..4, after the barrier), into slot slot_dma.  kSync >= 0: the stage barrier (with its wait for
+  // the next stage's data) comes after the MFMAs of rows 0..kSync, so that
+  // queued MFMAs cover it; every read of the step follows the barrier.
+  auto step = [&](auto sync_tag, bf16x8 (&a)[8], const bf16x8 (&bc)[4], bf16x8 (&bn)[4],
+                  int wsn, int hsn, int kkn, int dma, int s_dma, int slot_dma) {
+    constexpr int kSync = decltype(sync_tag)::value;
+    // Reads held back by the barrier (kSync >= 0), in this order: a[0..kSync],
+    // then bn[0..3]; row kSync + 1 + r takes item r after its second MFMA
+    // and, for r < kExtra, item kRows + r after its fourth.
+    constexpr int kRows = 7 - kSync;
+    constexpr int kItems = kSync + 5;
+    constexpr int kExtra = kItems - kRows > 0 ? kItems - kRows : 0;
+    auto held = [&](int item) {
+      if (item <= kSync) a[item] = rd_a(wsn, kkn, item);
+      else bn[item - kSync - 1] = rd_b(hsn, kkn, item - kSync - 1);
+    };
+    auto row = [&](int i) {
+      const int r = i - kSync - 1;
+      acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[0], acc[i][0], 0, 0, 0);
+      acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[1], acc[i][1], 0, 0, 0);
+      if (kSync < 0) {
+        if (i < 4) bn[i] = rd_b(hsn, kkn, i);
+      } else if (r >= 0 && r < kItems) {
+        held(r);
+      }
+      acc[i][2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[2], acc[i][2], 0, 0, 0);
+      acc[i][3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[3], acc[i][3], 0, 0, 0);
+      if (kSync < 0 || r >= 0) a[i] = rd_a(wsn, kkn, i);
+      if (kSync >= 0 && r >= 0 && r < kExtra) held(kRows + r);
+      if (dma == 1 && i < 4) issue_W1(s_dma, slot_dma, i);
+      if (dma == 2 && i >= 1 && i < 5) issue_H1(s_dma, slot_dma, i - 1);
+    };
+    auto order = [&](int i) {
+      const int r = i - kSync - 1;
+      const bool r1 = kSync < 0 ? i < 4 : (r >= 0 && r < kItems);
+      const int n2 = (kSync < 0 || r >= 0 ? 1 : 0) + (kSync >= 0 && r >= 0 && r < kExtra ? 1 : 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+      if (r1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      if (n2 >= 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (n2 >= 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if ((dma == 1 && i < 4) || (dma == 2 && i >= 1 && i < 5))
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // buffer load
+    };
+    if (kSync >= 0) {
+#pragma unroll
+      for (int i = 0; i <= kSync; ++i) row(i);
+#pragma unroll
+      for (int i = 0; i <= kSync; ++i) order(i);
+      __builtin_amdgcn_sched_barrier(0);
+      // the next stage's hidden and W resident; all reads of this stage returned
+      wait_vm_lgkm0<4>();
+      barrier_nofence();
+      __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int i = kSync + 1; i < 8; ++i) row(i);
+#pragma unroll
+    for (int i = kSync + 1; i < 8; ++i) order(i);
   };
+  using NoSync = std::integral_constant<int, -1>;
+  using SyncAfterRow0 = std::integral_constant<int, 0>;
 
-  bf16x8 a0[4], b0[2], a1[4], b1[2];
+  bf16x8 a[8], b0[4], b1[4];
   // Load order: H0 W0 W1 H1, then per stage k: W(k+2) during the stage's
-  // first two sub-steps, H(k+2) right after the stage's barrier.  At the
-  // barrier of stage k only W(k+2), the 4 newest loads, may be in flight, and
-  // every slot refilled after it belongs to a stage all waves have finished
-  // reading.  Stages past the end read as zero into slots nobody reads again.
+  // first K step, H(k+2) during its second, after the stage's barrier (which
+  // follows the second step's first four MFMAs).
+  // At the barrier of stage k only W(k+2), the 4 newest loads, may be in
+  // flight, and every slot refilled after it belongs to a stage all waves
+  // have finished reading.  Stages past the end read as zero into slots
+  // nobody reads again.
   issue_H(0, 0);
   issue_W(0, 0);
   issue_W(1, 1);
   issue_H(1, 1);
   wait_vm_lgkm0<8>();  // H0 and W0 resident
   barrier_nofence();
-  load_frags(0, 0, 0, a0, b0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = rd_a(0, 0, i);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) b0[j] = rd_b(0, 0, j);
   int ws = 0, hs = 0, ws2 = 2;  // W slots of stages k and k + 2, hidden slot of k
   for (int k = 0; k + 1 < nk; ++k) {
     const int ws1 = ws == 2 ? 0 : ws + 1, hs1 = hs ^ 1;
-    phase(a0, b0, ws, hs, 1, a1, b1, 2, k + 2, ws2);
+    step(NoSync{}, a, b0, b1, ws, hs, 1, 1, k + 2, ws2);
     __builtin_amdgcn_sched_barrier(0);
-    phase(a1, b1, ws, hs, 2, a0, b0, 3, k + 2, ws2);
-    __builtin_amdgcn_sched_barrier(0);
-    phase(a0, b0, ws, hs, 3, a1, b1, 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    // hidden and W of stage k+1 resident; all reads of stage k returned
-    wait_vm_lgkm0<4>();
-    barrier_nofence();
-    phase(a1, b1, ws1, hs1, 0, a0, b0, 1, k + 2, hs);
+    step(SyncAfterRow0{}, a, b1, b0, ws1, hs1, 0, 2, k + 2, hs);
     __builtin_amdgcn_sched_barrier(0);
     ws = ws1;
     hs = hs1;
     ws2 = ws2 == 2 ? 0 : ws2 + 1;
   }
-  phase(a0, b0, ws, hs, 1, a1, b1, 0, 0, 0);
-  phase(a1, b1, ws, hs, 2, a0, b0, 0, 0, 0);
-  phase(a0, b0, ws, hs, 3, a1, b1, 0, 0, 0);
+  step(NoSync{}, a, b0, b1, ws, hs, 1, 0, 0, 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b1[j], acc[i][j], 0, 0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
-  epilogue<kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+  epilogue<Acc16, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
 }
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
@@ -634,7 +706,7 @@ __device__ __forceinline__ void gemm_stats_f32_body(
     __syncthreads();
   }
 
-  epilogue<kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+  epilogue<Acc32, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
 }
 
 // Entry points: positions = hidden rows 0..M-1, or gathered through a row
