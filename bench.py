@@ -251,15 +251,15 @@ def measured_peaks(dev):
                                          ctypes.c_void_p]
     stream = torch.cuda.current_stream(dev).cuda_stream
     blocks, iters = 7904, 256      # the LM head's grid and K/16 at the LLaDA-8B shape
-    flops = blocks * 8.0 * iters * 8 * 32768
+    flops = blocks * 8.0 * iters * 16 * 16384
     out = torch.empty(blocks * 512, device=dev)
     # operands drawn like the LM head's data: W_head N(0, 1/d) and hidden
     # rows N(0, 1) x RMS U[0.5, 2] (d = 4096), bf16
     nfrag = 1024
     gen = torch.Generator(device=dev).manual_seed(0xF00D)
-    a_src = (torch.randn(nfrag * 12 * 64 * 8, generator=gen, device=dev) / 64.0).to(torch.bfloat16)
-    b_src = (torch.randn(nfrag * 12 * 64 * 8, generator=gen, device=dev) *
-             (0.5 + 1.5 * torch.rand(nfrag * 12 * 64 * 8, generator=gen, device=dev))
+    a_src = (torch.randn(nfrag * 16 * 64 * 8, generator=gen, device=dev) / 64.0).to(torch.bfloat16)
+    b_src = (torch.randn(nfrag * 8 * 64 * 8, generator=gen, device=dev) *
+             (0.5 + 1.5 * torch.rand(nfrag * 8 * 64 * 8, generator=gen, device=dev))
              ).to(torch.bfloat16)
 
     def const():
@@ -303,10 +303,11 @@ def measured_peaks(dev):
     del src, dst
     return {"mfma_bf16_TFLOP_s": mfma_data, "mfma_bf16_TFLOP_s_constant_operands": mfma,
             "hbm_copy_GB_s": hbm,
-            "how": "MFMA: 7904 workgroups x 8 waves x 256 rounds of 8 independent "
-                   "v_mfma_f32_32x32x16_bf16 on register operands (the flops of one LM-head "
-                   "launch), operands alternating between two sets of fragments loaded from "
-                   "random bf16 data drawn like W_head and the hidden rows (the rate quoted), "
+            "how": "MFMA: 7904 workgroups x 8 waves x 256 rounds of 16 independent "
+                   "v_mfma_f32_16x16x32_bf16 (the LM-head kernel's instruction) on register "
+                   "operands (the flops of one LM-head launch), operands alternating between two "
+                   "sets of fragments loaded from random bf16 data drawn like W_head and the "
+                   "hidden rows (the rate quoted), "
                    "and on one constant set (constant_operands); best of five rounds of four "
                    "launches, the two probes alternating; HBM: streaming copy of 1 GiB "
                    "(4 x 16 B per thread per iteration), read + write counted, 5 repetitions"}

@@ -479,20 +479,23 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
       for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
 
   // Fragments of one 32-element K step: A fragment i = W rows arow + 16 i,
-  // B fragment j = positions brow + 16 j; lane group kq = lane / 16 supplies
-  // 16-byte chunk kq of the step (the same chunk of both operands, so each
-  // MFMA sums over the step's 32 K values).  Rows 16 apart share a swizzle.
+  // B fragment j = positions brow + 16 j.  Step kk of a stage takes the
+  // stage's 16-byte chunks kk, kk + 2, kk + 4, kk + 6: lane group kq =
+  // lane / 16 supplies chunk 2 kq + kk of both operands, so each MFMA sums
+  // over the step's 32 K values and the two steps cover the stage.  With the
+  // swizzle above, this assignment reads LDS without bank conflicts (four
+  // consecutive chunks per step do not).  Rows 16 apart share a swizzle.
   const int arow = wv * 128 + (lane & 15);
   const int brow = wp * 64 + (lane & 15);
   const int kq = lane >> 4;
   const int fa = swz(arow), fb = swz(brow);
   auto rd_a = [&](int ws, int kk, int i) {
-    const int chunk = kk * 4 + kq;
+    const int chunk = 2 * kq + kk;
     return *reinterpret_cast<const bf16x8*>(smem + ws * kOperandBytes + (arow + 16 * i) * kSlab +
                                             ((chunk ^ fa) << 4));
   };
   auto rd_b = [&](int hs, int kk, int j) {
-    const int chunk = kk * 4 + kq;
+    const int chunk = 2 * kq + kk;
     return *reinterpret_cast<const bf16x8*>(smem + (3 + hs) * kOperandBytes +
                                             (brow + 16 * j) * kSlab + ((chunk ^ fb) << 4));
   };
@@ -500,7 +503,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   // MFMAs of row i, a[i] is refilled with the fragment of step kkn (slots
   // wsn / hsn), and the four bn are read in between.  `dma` spreads four
   // buffer loads over the rows: 1 = W stage s_dma (rows 0..3), 2 = hidden
-  // stage s_dma (rows 1..4, after the barrier), into slot slot_dma.  kSync >= 0: the stage barrier (with its wait for
+  // stage s_dma (rows 2..5, after the barrier), into slot slot_dma.  kSync >= 0: the stage barrier (with its wait for
   // the next stage's data) comes after the MFMAs of rows 0..kSync, so that
   // queued MFMAs cover it; every read of the step follows the barrier.
   auto step = [&](auto sync_tag, bf16x8 (&a)[8], const bf16x8 (&bc)[4], bf16x8 (&bn)[4],
@@ -530,7 +533,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
       if (kSync < 0 || r >= 0) a[i] = rd_a(wsn, kkn, i);
       if (kSync >= 0 && r >= 0 && r < kExtra) held(kRows + r);
       if (dma == 1 && i < 4) issue_W1(s_dma, slot_dma, i);
-      if (dma == 2 && i >= 1 && i < 5) issue_H1(s_dma, slot_dma, i - 1);
+      if (dma == 2 && i >= 2 && i < 6) issue_H1(s_dma, slot_dma, i - 2);
     };
     auto order = [&](int i) {
       const int r = i - kSync - 1;
@@ -541,7 +544,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       if (n2 >= 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (n2 >= 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      if ((dma == 1 && i < 4) || (dma == 2 && i >= 1 && i < 5))
+      if ((dma == 1 && i < 4) || (dma == 2 && i >= 2 && i < 6))
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // buffer load
     };
     if (kSync >= 0) {
@@ -561,12 +564,12 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     for (int i = kSync + 1; i < 8; ++i) order(i);
   };
   using NoSync = std::integral_constant<int, -1>;
-  using SyncAfterRow0 = std::integral_constant<int, 0>;
+  using SyncAfterRow1 = std::integral_constant<int, 1>;
 
   bf16x8 a[8], b0[4], b1[4];
   // Load order: H0 W0 W1 H1, then per stage k: W(k+2) during the stage's
   // first K step, H(k+2) during its second, after the stage's barrier (which
-  // follows the second step's first four MFMAs).
+  // follows the second step's first eight MFMAs).
   // At the barrier of stage k only W(k+2), the 4 newest loads, may be in
   // flight, and every slot refilled after it belongs to a stage all waves
   // have finished reading.  Stages past the end read as zero into slots
@@ -586,7 +589,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     const int ws1 = ws == 2 ? 0 : ws + 1, hs1 = hs ^ 1;
     step(NoSync{}, a, b0, b1, ws, hs, 1, 1, k + 2, ws2);
     __builtin_amdgcn_sched_barrier(0);
-    step(SyncAfterRow0{}, a, b1, b0, ws1, hs1, 0, 2, k + 2, hs);
+    step(SyncAfterRow1{}, a, b1, b0, ws1, hs1, 0, 2, k + 2, hs);
     __builtin_amdgcn_sched_barrier(0);
     ws = ws1;
     hs = hs1;
