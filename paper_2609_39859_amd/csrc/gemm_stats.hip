@@ -191,6 +191,27 @@ struct Acc32 {
 // What the epilogue produces besides the per-tile statistics.
 enum EpilogueMode { kGreedy = 0, kDrawn = 1, kTarget = 2 };
 
+// Per-position inputs of the epilogue, loaded before the last MFMAs so that
+// their latency is hidden: the given token (kTarget) or the draw's row index
+// (kDrawn) of each column this lane holds.
+template <class Lay>
+struct ColIn {
+  int col[Lay::kNJ];
+};
+
+template <class Lay, int kMode>
+__device__ __forceinline__ void load_col_inputs(ColIn<Lay>& ci, int tid, int lane, int wp, int p0,
+                                                int M, const SampleArgs& sa,
+                                                const TargetArgs& ta) {
+  if (kMode == kGreedy) return;
+  const int32_t* src = kMode == kTarget ? ta.token : sa.row;
+#pragma unroll
+  for (int j = 0; j < Lay::kNJ; ++j) {
+    const int p = p0 + wp * 64 + Lay::col(j, lane);
+    ci.col[j] = p < M ? src[p] : -1;
+  }
+}
+
 // Statistics of the logits of column j that this lane holds (rows vbase +
 // Lay::row(i, e, lane), increasing in (i, e)), combined with the lanes that
 // hold the column's other rows: the maximum m, the lowest row holding it,
@@ -265,13 +286,15 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
                                               int tid, int lane, int wv, int wp, int vt, int v0,
                                               int p0, int M, int V,
                                               float4* __restrict__ partials, const SampleArgs& sa,
-                                              const TargetArgs& ta) {
+                                              const TargetArgs& ta, const ColIn<Lay>& ci) {
   constexpr bool kDraw = kMode == kDrawn;
   constexpr bool full = kFull;
   float4* red = reinterpret_cast<float4*>(smem);  // [2][kTileP]
   float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
   const int vbase = v0 + wv * 128;
   const bool leader = lane < Lay::kLeaders;
+  // the draw's row of position p0 + tid, for the store after the exchange
+  const int own_row = (kDraw && tid < kTileP && p0 + tid < M) ? sa.row[p0 + tid] : -1;
 #pragma unroll
   for (int j = 0; j < Lay::kNJ; ++j) {
     float m, s, t;
@@ -280,7 +303,7 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
     const int col = wp * 64 + Lay::col(j, lane);
     if (leader) red[wv * kTileP + col] = make_float4(m, s, t, __int_as_float(idx));
     if (kMode == kTarget) {
-      const int tk = p0 + col < M ? ta.token[p0 + col] : -1;
+      const int tk = ci.col[j];
       if (tk >= vbase && tk < vbase + 128 && tk < V) {
         float zt = 0.f;
         bool hit = false;
@@ -296,7 +319,7 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
       }
     }
     if (kDraw) {
-      const int srow = p0 + col < M ? sa.row[p0 + col] : -1;
+      const int srow = ci.col[j];
       if (__ballot(srow >= 0)) {
         float best = -INFINITY, bz = 0.f;
         int bidx = 0x7fffffff;
@@ -344,7 +367,7 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
     const int r = p0 + tid;
     if (r < M) {
       partials[(size_t)vt * M + r] = merge2(red[tid], red[kTileP + tid]);
-      if (kDraw && sa.row[r] >= 0) {
+      if (kDraw && own_row >= 0) {
         const float4 a = sred[tid], b = sred[kTileP + tid];
         const bool take_a = a.x > b.x || (a.x == b.x && __float_as_int(a.y) < __float_as_int(b.y));
         sa.partials[(size_t)vt * M + r] = make_float4(take_a ? a.x : b.x, take_a ? a.y : b.y,
@@ -358,13 +381,14 @@ template <class Lay, int kMode>
 __device__ __forceinline__ void epilogue(typename Lay::Arr& acc, unsigned char* smem, int tid,
                                          int lane, int wv, int wp, int vt, int v0, int p0, int M,
                                          int V, float4* __restrict__ partials,
-                                         const SampleArgs& sa, const TargetArgs& ta) {
+                                         const SampleArgs& sa, const TargetArgs& ta,
+                                         const ColIn<Lay>& ci) {
   if (v0 + kTileV <= V)
     epilogue_tile<Lay, kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa,
-                                    ta);
+                                    ta, ci);
   else
     epilogue_tile<Lay, kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials,
-                                     sa, ta);
+                                     sa, ta, ci);
 }
 
 __device__ __forceinline__ void barrier_nofence() {
@@ -595,6 +619,8 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     hs = hs1;
     ws2 = ws2 == 2 ? 0 : ws2 + 1;
   }
+  ColIn<Acc16> ci;
+  load_col_inputs<Acc16, kMode>(ci, tid, lane, wp, p0, M, sa, ta);
   step(NoSync{}, a, b0, b1, ws, hs, 1, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -604,7 +630,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
-  epilogue<Acc16, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+  epilogue<Acc16, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta, ci);
 }
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
@@ -709,7 +735,9 @@ __device__ __forceinline__ void gemm_stats_f32_body(
     __syncthreads();
   }
 
-  epilogue<Acc32, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta);
+  ColIn<Acc32> ci;
+  load_col_inputs<Acc32, kMode>(ci, tid, lane, wp, p0, M, sa, ta);
+  epilogue<Acc32, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta, ci);
 }
 
 // Entry points: positions = hidden rows 0..M-1, or gathered through a row
