@@ -40,7 +40,7 @@
 // reads of the next step are interleaved with the current MFMAs, and the
 // buffer loads of later stages are spread over the stage one at a time so
 // that no wave stalls its MFMA stream behind a burst of loads.  The 16x16x32
-// MFMA shape moves the same bytes per flop as 32x32x16 and, on this GPU,
+// MFMA shape moves the same bytes per flop as 32x32x16 and, on gfx950,
 // sustains a higher clock under the same power limit.
 // fp32 path (small problems): register-staged double buffer.
 //
