@@ -527,9 +527,10 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   // MFMAs of row i, a[i] is refilled with the fragment of step kkn (slots
   // wsn / hsn), and the four bn are read in between.  `dma` spreads four
   // buffer loads over the rows: 1 = W stage s_dma (rows 0..3), 2 = hidden
-  // stage s_dma (rows 2..5, after the barrier), into slot slot_dma.  kSync >= 0: the stage barrier (with its wait for
-  // the next stage's data) comes after the MFMAs of rows 0..kSync, so that
-  // queued MFMAs cover it; every read of the step follows the barrier.
+  // stage s_dma (rows 2..5, after the barrier), into slot slot_dma.
+  // kSync >= 0: the stage barrier (with its wait for the next stage's data)
+  // comes after the MFMAs of rows 0..kSync, so that queued MFMAs cover it;
+  // every read of the step follows the barrier.
   auto step = [&](auto sync_tag, bf16x8 (&a)[8], const bf16x8 (&bc)[4], bf16x8 (&bn)[4],
                   int wsn, int hsn, int kkn, int dma, int s_dma, int slot_dma) {
     constexpr int kSync = decltype(sync_tag)::value;
