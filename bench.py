@@ -245,7 +245,7 @@ def measured_peaks(dev):
     lib = ctypes.CDLL(PROBE_LIB)
     lib.fork_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     lib.fork_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                    ctypes.c_int, ctypes.c_void_p]
+                                    ctypes.c_void_p]
     lib.fork_probe_mfma_data.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                          ctypes.c_void_p]
@@ -290,12 +290,12 @@ def measured_peaks(dev):
     n = (1 << 30) // 16
     src = torch.ones(n * 16, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
-    assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, 4096, stream) == 0
+    assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, stream) == 0
     torch.cuda.synchronize()
     reps = 5
     start.record()
     for _ in range(reps):
-        assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, 4096, stream) == 0
+        assert lib.fork_probe_copy(src.data_ptr(), dst.data_ptr(), n, stream) == 0
     stop.record()
     torch.cuda.synchronize()
     assert bool(dst[-1] == 1)
@@ -310,7 +310,8 @@ def measured_peaks(dev):
                    "hidden rows (the rate quoted), "
                    "and on one constant set (constant_operands); best of five rounds of four "
                    "launches, the two probes alternating; HBM: streaming copy of 1 GiB "
-                   "(4 x 16 B per thread per iteration), read + write counted, 5 repetitions"}
+                   "(one 16-byte element per thread, nontemporal loads and stores), read + "
+                   "write counted, 5 repetitions"}
 
 
 def selection(args, dev):

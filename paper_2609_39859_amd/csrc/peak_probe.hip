@@ -101,20 +101,14 @@ __global__ __launch_bounds__(512) void mfma_data_kernel(int iters, const bf16x8*
   out[blockIdx.x * 512 + threadIdx.x] = s;
 }
 
-// Streaming copy: each thread moves four 16-byte elements per iteration
-// (consecutive threads on consecutive elements), grid-stride.
-__global__ __launch_bounds__(256) void stream_copy_kernel(const uint4* __restrict__ src,
-                                                          uint4* __restrict__ dst, size_t n) {
-  const size_t stride = (size_t)gridDim.x * 1024;
-  for (size_t i = (size_t)blockIdx.x * 1024 + threadIdx.x; i < n; i += stride) {
-    uint4 v[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (i + 256 * j < n) v[j] = src[i + 256 * j];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (i + 256 * j < n) dst[i + 256 * j] = v[j];
-  }
+// Streaming copy: one 16-byte element per thread over a grid that covers the
+// buffer, nontemporal loads and stores (of the copy forms tried — several
+// elements per thread, grid-stride loops, cached accesses — the fastest).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(256) void stream_copy_kernel(const u32x4* __restrict__ src,
+                                                          u32x4* __restrict__ dst, size_t n) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
 }  // namespace
@@ -145,11 +139,15 @@ int fork_probe_mfma_data(int blocks, int iters, const void* a_src, const void* b
 }
 
 // Launches the copy probe on n 16-byte elements (src and dst 16-byte
-// aligned, n * 16 bytes each).  Returns a hipError_t.
-int fork_probe_copy(const void* src, void* dst, size_t n, int blocks, void* stream) {
+// aligned, n * 16 bytes each, n < 2^39): ceil(n / 256) workgroups.  Returns
+// a hipError_t.
+int fork_probe_copy(const void* src, void* dst, size_t n, void* stream) {
+  const size_t blocks = (n + 255) / 256;
+  if (blocks == 0) return (int)hipSuccess;
+  if (blocks > 0x7fffffffu) return (int)hipErrorInvalidValue;
   hipLaunchKernelGGL(stream_copy_kernel, dim3((unsigned)blocks), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), static_cast<const uint4*>(src),
-                     static_cast<uint4*>(dst), n);
+                     static_cast<hipStream_t>(stream), static_cast<const u32x4*>(src),
+                     static_cast<u32x4*>(dst), n);
   return (int)hipGetLastError();
 }
 
