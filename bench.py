@@ -323,9 +323,9 @@ def selection(args, dev):
     position): algorithmic bytes per sequence = block start, the block's 32
     mask bytes and 32 confidences read, the committed candidate read, and
     token, mask byte, fallback flag and block start written.  The timed
-    launches cycle over enough distinct copies of the batch that together
-    they exceed twice the 256 MB last-level cache, so the bytes come from
-    HBM, not from the cache."""
+    launches cycle over enough distinct copies of the batch that the bytes
+    one launch touches, summed over the copies, exceed twice the 256 MB
+    last-level cache, so they come from HBM, not from the cache."""
     import torch
 
     from paper_2609_39859_amd import _binding
@@ -379,9 +379,10 @@ def selection(args, dev):
     for name, B, L, BL in (("llada8b", 8, 512, 32), ("rollout", 64, 384, 32),
                            ("long", 2, 2048, 64)):
         out["latency_us"][name] = run(B, L, BL, 20, 3)
-    set_bytes_per_seq = 32 * (4 + 4 + 4 + 1) + 4 + 4  # conf, candidates, tokens, mask, state
     for B in (1 << 14, 1 << 17, 1 << 20):
-        nsets = max(1, -(-(512 << 20) // (set_bytes_per_seq * B)))
+        # enough copies that the bytes one launch touches, summed over the
+        # copies, exceed twice the last-level cache
+        nsets = max(1, -(-(512 << 20) // (SEL_BYTES_PER_SEQ * B)))
         reps = max(20, nsets)
         assert 3 + 2 * -(-reps // nsets) < 32   # each copy keeps masked positions
         for layout, lname in ((_binding.FORK_LAYOUT_ROW_MAJOR, "row_major"),
@@ -391,7 +392,7 @@ def selection(args, dev):
             out["sweep"].append({"B": B, "L": 32, "block_len": 32, "layout": lname, "us": us,
                                  "GB_s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
                                  "bytes_per_seq": SEL_BYTES_PER_SEQ, "batch_copies": nsets,
-                                 "bytes_cycled": nsets * set_bytes_per_seq * B})
+                                 "bytes_touched_cycled": nsets * SEL_BYTES_PER_SEQ * B})
     return out
 
 

@@ -83,8 +83,8 @@ hipError_t launch_active_rows(int B, int L, int block_len, const uint8_t* mask,
 // least kLaneSelectMinB sequences with blocks of at most kLaneSelectMaxBL
 // positions run one lane per sequence, others one wave per sequence.
 // Position-major state (at k * B + b): one lane per four sequences from
-// kPmWideMinB sequences on, one lane per sequence below.  All give the same
-// results.
+// kPmWideMinB sequences on (B a multiple of 4, the arrays 16-byte aligned),
+// one lane per sequence otherwise.  All give the same results.
 constexpr int kLaneSelectMinB = 4096;
 constexpr int kLaneSelectMaxBL = 64;
 constexpr int kPmWideMinB = 1 << 18;

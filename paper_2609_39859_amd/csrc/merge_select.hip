@@ -25,6 +25,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace fork {
 namespace {
 
@@ -607,11 +609,20 @@ __global__ __launch_bounds__(256) void select_lanes_kernel(
 // small batches still spread over many waves).  When the group shares its
 // block start and the block has at most 32 positions, each position of the
 // block comes in as one load of the group's kS confidences (and keys) and
-// one of its kS mask bytes, so a wave's loads cover whole cache lines; the
-// loads are issued kChunk positions at a time before any is used, and the
-// rule is decided on 32-bit masks in registers.  Sequences outside that case
-// take the position-by-position path.  Decisions are those of the row-major
-// kernels.
+// one of its kS mask bytes, so a wave's loads cover whole cache lines.
+// Loads are issued kChunk positions at a time, with the next batch in flight
+// while one is decided when kDB; every load is unconditional (positions past
+// the block re-read its last one and are ignored), so the compiler counts
+// the loads in flight instead of waiting for all of them.  Confidences, keys
+// and mask bytes are read once, with nontemporal loads.  The rule class is a
+// template parameter: the threshold, leftmost and random rules load no keys.
+// For kS = 4, when the group's four sequences each commit one position, the
+// same one, the candidates, tokens and mask bytes move as one 16-byte and one
+// 4-byte access, and the per-sequence outputs are stored as 16-byte vectors
+// (the host launches kS = 4 only when every array is aligned for that).
+// Sequences outside these cases take the position-by-position path.
+// Decisions are those of the row-major kernels.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 template <int kS> struct PmVec;
 template <> struct PmVec<1> {
   typedef float F;
@@ -619,14 +630,12 @@ template <> struct PmVec<1> {
   static __device__ float get(F v, int) { return v; }
 };
 template <> struct PmVec<4> {
-  typedef float4 F;
+  typedef f32x4 F;
   typedef uint32_t M;
-  static __device__ float get(F v, int j) {
-    return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
-  }
+  static __device__ float get(F v, int j) { return v[j]; }
 };
 
-template <int kS, int kChunk>
+template <int kS, int kChunk, bool kDB, bool kExtreme>
 __global__ __launch_bounds__(256) void select_pm_kernel(
     int B, int L, int BL, float tau, int rule, const float* __restrict__ conf,
     const float* __restrict__ entropy, const float* __restrict__ uniform,
@@ -636,26 +645,37 @@ __global__ __launch_bounds__(256) void select_pm_kernel(
     int32_t* __restrict__ commit_pos) {
   typedef typename PmVec<kS>::F VF;
   typedef typename PmVec<kS>::M VM;
+  static_assert(kS == 1 || kS == 4, "one or four sequences per lane");
   const int b0 = kS * (blockIdx.x * 256 + threadIdx.x);
   if (b0 >= B) return;
   const PosMajor at{B};
-  const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
   const float* key = rule == kMaxEnt ? entropy : conf;
-  bool wide = b0 + kS <= B && (B % kS) == 0 && BL <= 32 &&
-              ((reinterpret_cast<uintptr_t>(conf) | reinterpret_cast<uintptr_t>(key)) &
-               (sizeof(VF) - 1)) == 0 &&
-              (reinterpret_cast<uintptr_t>(mask) & (sizeof(VM) - 1)) == 0;
-  int s = 0;
-  if (wide) {
-    s = block_start[b0];
-    for (int j = 1; j < kS; ++j) wide = wide && block_start[b0 + j] == s;
-    wide = wide && s >= 0 && s + BL <= L;
+  const bool lowest = rule == kMinConf;
+  // the group's block starts in one load (kS = 4: B % 4 == 0, 16-byte aligned)
+  int sv[kS];
+  if (kS == 4) {
+    const int4 v = *reinterpret_cast<const int4*>(block_start + b0);
+    sv[0] = v.x;
+    sv[kS > 1 ? 1 : 0] = v.y;
+    sv[kS > 2 ? 2 : 0] = v.z;
+    sv[kS > 3 ? 3 : 0] = v.w;
+  } else {
+    sv[0] = block_start[b0];
   }
+  const int s = sv[0];
+  int differ = 0;
+#pragma unroll
+  for (int j = 1; j < kS; ++j) differ |= sv[j] ^ s;
+  // no short-circuit: the compiler would otherwise split the load above
+  const bool wide = (differ == 0) & (s >= 0) & (s + BL <= L) & (BL <= 32);
   if (!wide) {
-    for (int b = b0; b < min(b0 + kS, B); ++b)
-      lane_rule(b, block_start[b], L, BL, tau, rule, conf, entropy, uniform, argmax, tokens,
-                mask, block_start, fallback, ncommit,
+#pragma unroll 1
+    for (int j = 0; j < kS; ++j) {
+      const int b = b0 + j;
+      lane_rule(b, sv[j], L, BL, tau, rule, conf, entropy, uniform, argmax, tokens, mask,
+                block_start, fallback, ncommit,
                 commit_pos ? commit_pos + (size_t)b * BL : nullptr, at);
+    }
     return;
   }
   uint32_t mb[kS], pb[kS];
@@ -667,37 +687,110 @@ __global__ __launch_bounds__(256) void select_pm_kernel(
     best[j] = 0.f;
     bi[j] = -1;
   }
-  const bool lowest = rule == kMinConf;
-  for (int i0 = 0; i0 < BL; i0 += kChunk) {
-    VM mv[kChunk];
-    VF cv[kChunk], kv[kChunk];
+  VM mv[2][kChunk];
+  VF cv[2][kChunk], kv[2][kChunk];
+  auto load = [&](auto bufc, int i0) {
+    constexpr int buf = decltype(bufc)::value;
 #pragma unroll
     for (int u = 0; u < kChunk; ++u) {
-      if (i0 + u < BL) {
-        const size_t row = (size_t)(s + i0 + u) * B + b0;
-        mv[u] = *reinterpret_cast<const VM*>(mask + row);
-        cv[u] = *reinterpret_cast<const VF*>(conf + row);
-        if (extreme) kv[u] = *reinterpret_cast<const VF*>(key + row);
-      }
+      // positions past the block re-read its last one (in bounds, ignored)
+      const size_t row = (size_t)(s + min(i0 + u, BL - 1)) * B + b0;
+      mv[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const VM*>(mask + row));
+      cv[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const VF*>(conf + row));
+      if (kExtreme) kv[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const VF*>(key + row));
     }
+  };
+  auto decide = [&](auto bufc, int i0) {
+    constexpr int buf = decltype(bufc)::value;
 #pragma unroll
     for (int u = 0; u < kChunk; ++u) {
       const int i = i0 + u;
-      if (i >= BL) break;
+      const bool in = i < BL;
 #pragma unroll
       for (int j = 0; j < kS; ++j) {
-        const bool m = (((uint32_t)mv[u] >> (8 * j)) & 0xffu) != 0;
-        const float c = PmVec<kS>::get(cv[u], j);
-        const float k = extreme ? PmVec<kS>::get(kv[u], j) : c;
-        mb[j] |= (uint32_t)m << i;
-        pb[j] |= (uint32_t)(m && c > tau) << i;
-        // branch-free: a select per value (lowest position on equal keys)
-        const bool better = lowest ? k < best[j] : k > best[j];
-        const bool take = extreme && m && (bi[j] < 0 || better);
-        best[j] = take ? k : best[j];
-        bi[j] = take ? i : bi[j];
+        const bool m = in & ((((uint32_t)mv[buf][u] >> (8 * j)) & 0xffu) != 0);
+        const float c = PmVec<kS>::get(cv[buf][u], j);
+        mb[j] |= (uint32_t)m << (i & 31);
+        pb[j] |= (uint32_t)(m & (c > tau)) << (i & 31);
+        if (kExtreme) {
+          // branch-free: a select per value (lowest position on equal keys)
+          const float k = PmVec<kS>::get(kv[buf][u], j);
+          const bool better = lowest ? k < best[j] : k > best[j];
+          const bool take = m & ((bi[j] < 0) | better);
+          best[j] = take ? k : best[j];
+          bi[j] = take ? i : bi[j];
+        }
       }
     }
+  };
+  using Buf0 = std::integral_constant<int, 0>;
+  using Buf1 = std::integral_constant<int, 1>;
+  if (kDB) {
+    load(Buf0{}, 0);
+    for (int i0 = 0; i0 < BL; i0 += 2 * kChunk) {
+      load(Buf1{}, i0 + kChunk);
+      decide(Buf0{}, i0);
+      load(Buf0{}, i0 + 2 * kChunk);
+      decide(Buf1{}, i0 + kChunk);
+    }
+  } else {
+    for (int i0 = 0; i0 < BL; i0 += kChunk) {
+      load(Buf0{}, i0);
+      decide(Buf0{}, i0);
+    }
+  }
+  // positions to commit and the fallback flag of each sequence
+  uint32_t commit[kS];
+  int fbv[kS];
+  bool any_empty = false;
+#pragma unroll
+  for (int j = 0; j < kS; ++j) {
+    any_empty = any_empty || mb[j] == 0;
+    const bool fb = pb[j] == 0;
+    commit[j] = pb[j];
+    fbv[j] = fb ? 1 : 0;
+    if (fb && mb[j] != 0) {
+      int pick;
+      if (rule == kLeftmost) {
+        pick = __ffs(mb[j]) - 1;
+      } else if (rule == kRandom) {
+        const int n = __popc(mb[j]);
+        int r = (int)(uniform[b0 + j] * (float)n);
+        r = r > n - 1 ? n - 1 : (r < 0 ? 0 : r);
+        uint32_t rest = mb[j];
+        for (int t = 0; t < r; ++t) rest &= rest - 1;  // drop the r lowest
+        pick = __ffs(rest) - 1;
+      } else {
+        pick = bi[j];
+      }
+      commit[j] = 1u << pick;
+    }
+  }
+  if (kS == 4 && !any_empty && commit_pos == nullptr) {
+    bool same1 = (commit[0] & (commit[0] - 1)) == 0;
+#pragma unroll
+    for (int j = 1; j < kS; ++j) same1 = same1 && commit[j] == commit[0];
+    if (same1) {
+      const size_t row = (size_t)(s + __ffs(commit[0]) - 1) * B + b0;
+      *reinterpret_cast<int4*>(tokens + row) = *reinterpret_cast<const int4*>(argmax + row);
+      *reinterpret_cast<uint32_t*>(mask + row) = 0u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < kS; ++j)
+        for (uint32_t rest = commit[j]; rest; rest &= rest - 1) {
+          const size_t idx = at(b0 + j, s + __ffs(rest) - 1);
+          tokens[idx] = argmax[idx];
+          mask[idx] = 0;
+        }
+    }
+    *reinterpret_cast<int4*>(fallback + b0) =
+        make_int4(fbv[0], fbv[kS > 1 ? 1 : 0], fbv[kS > 2 ? 2 : 0], fbv[kS > 3 ? 3 : 0]);
+    *reinterpret_cast<int4*>(block_start + b0) = make_int4(s, s, s, s);
+    if (ncommit)
+      *reinterpret_cast<int4*>(ncommit + b0) =
+          make_int4(__popc(commit[0]), __popc(commit[kS > 1 ? 1 : 0]),
+                    __popc(commit[kS > 2 ? 2 : 0]), __popc(commit[kS > 3 ? 3 : 0]));
+    return;
   }
 #pragma unroll
   for (int j = 0; j < kS; ++j) {
@@ -708,26 +801,8 @@ __global__ __launch_bounds__(256) void select_pm_kernel(
                 block_start, fallback, ncommit, my_commits, at);
       continue;
     }
-    const bool fb = pb[j] == 0;
-    uint32_t commit = pb[j];
-    if (fb) {
-      int pick;
-      if (rule == kLeftmost) {
-        pick = __ffs(mb[j]) - 1;
-      } else if (rule == kRandom) {
-        const int n = __popc(mb[j]);
-        int r = (int)(uniform[b] * (float)n);
-        r = r > n - 1 ? n - 1 : (r < 0 ? 0 : r);
-        uint32_t rest = mb[j];
-        for (int t = 0; t < r; ++t) rest &= rest - 1;  // drop the r lowest
-        pick = __ffs(rest) - 1;
-      } else {
-        pick = bi[j];
-      }
-      commit = 1u << pick;
-    }
     int written = 0;
-    for (uint32_t rest = commit; rest; rest &= rest - 1) {
+    for (uint32_t rest = commit[j]; rest; rest &= rest - 1) {
       const int k = s + __ffs(rest) - 1;
       const size_t idx = at(b, k);
       tokens[idx] = argmax[idx];
@@ -737,7 +812,7 @@ __global__ __launch_bounds__(256) void select_pm_kernel(
     }
     if (my_commits)
       for (int i = written; i < BL; ++i) my_commits[i] = -1;
-    fallback[b] = fb ? 1 : 0;
+    fallback[b] = fbv[j];
     block_start[b] = s;
     if (ncommit) ncommit[b] = written;
   }
@@ -806,14 +881,26 @@ hipError_t launch_select(int B, int L, int block_len, float tau, int rule,
                          const int32_t* argmax, int32_t* tokens, uint8_t* mask,
                          int32_t* block_start, int32_t* fallback, int32_t* ncommit,
                          int32_t* commit_pos, bool position_major, hipStream_t stream) {
-  if (position_major && B >= kPmWideMinB)
-    hipLaunchKernelGGL((select_pm_kernel<4, 4>), dim3((unsigned)(((B + 3) / 4 + 255) / 256)),
-                       dim3(256), 0, stream, B, L, block_len, tau, rule, conf, entropy, uniform,
-                       argmax, tokens, mask, block_start, fallback, ncommit, commit_pos);
-  else if (position_major)
-    hipLaunchKernelGGL((select_pm_kernel<1, 16>), dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
-                       stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
-                       tokens, mask, block_start, fallback, ncommit, commit_pos);
+  if (position_major) {
+    const bool extreme = rule == kMaxConf || rule == kMinConf || rule == kMaxEnt;
+    // four sequences per lane: whole 16-byte groups, every array aligned
+    auto a16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    const bool four = B >= kPmWideMinB && B % 4 == 0 && a16(conf) && a16(argmax) &&
+                      a16(tokens) && a16(block_start) && a16(fallback) &&
+                      (ncommit == nullptr || a16(ncommit)) &&
+                      (rule != kMaxEnt || a16(entropy)) &&
+                      (reinterpret_cast<uintptr_t>(mask) & 3) == 0;
+    const dim3 grid((unsigned)(((four ? B / 4 : B) + 255) / 256));
+#define FORK_SELECT_PM(S, C, D, X)                                                          \
+  hipLaunchKernelGGL((select_pm_kernel<S, C, D, X>), grid, dim3(256), 0, stream, B, L,       \
+                     block_len, tau, rule, conf, entropy, uniform, argmax, tokens, mask,     \
+                     block_start, fallback, ncommit, commit_pos)
+    if (four && extreme) FORK_SELECT_PM(4, 1, true, true);
+    else if (four) FORK_SELECT_PM(4, 1, true, false);
+    else if (extreme) FORK_SELECT_PM(1, 16, false, true);
+    else FORK_SELECT_PM(1, 16, false, false);
+#undef FORK_SELECT_PM
+  }
   else if (B >= kLaneSelectMinB && block_len <= kLaneSelectMaxBL)
     hipLaunchKernelGGL(select_lanes_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
                        stream, B, L, block_len, tau, rule, conf, entropy, uniform, argmax,
