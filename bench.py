@@ -747,7 +747,7 @@ def main():
         # Candidates drawn at sampling temperature 0.8 (Gumbel-max over
         # Philox4x32-10 draws for the active blocks' positions).
         drawn = {"temperature": 0.8}
-        for label, mode, kernel in (("all_rows", _binding.FORK_ROWS_ALL, "gemm_stats_bf16_draw_kernel"),
+        for label, mode, kernel in (("all_rows", _binding.FORK_ROWS_ALL, "gemm_stats_bf16_draw_ilv_kernel"),
                                     ("active_rows", _binding.FORK_ROWS_ACTIVE,
                                      "gemm_stats_bf16_rows_draw_kernel")):
             print("bench: timing %d steps, drawn candidates, %s" % (args.steps, label),

@@ -199,15 +199,34 @@ struct ColIn {
   int col[Lay::kNJ];
 };
 
+// Launch position of column c (0..255) of position tile pt.  Contiguous:
+// p0 + c.  Interleaved (M = 256 * npt, the drawing kernel over all rows):
+// 16-column block k of tile pt is the 16-row chunk k * npt + (pt + k) mod
+// npt, i.e. column c is row of that chunk's c % 16-th; chunk k * npt + s
+// goes to tile (s - k) mod npt.  The active blocks, the only rows whose
+// candidates are drawn, usually sit at a fixed offset in every sequence;
+// the rotation by k spreads them over the position tiles instead of
+// gathering them in a few (which a plain stride of npt chunks does whenever
+// the sequence length is a multiple of 16 npt), so the tiles' epilogues
+// cost about the same.
+struct PosMap {
+  int p0, pt, npt;
+  bool ilv;
+  __device__ int operator()(int c) const {
+    const int k = c >> 4;
+    return ilv ? ((k * npt + (pt + k) % npt) << 4) + (c & 15) : p0 + c;
+  }
+};
+
 template <class Lay, int kMode>
-__device__ __forceinline__ void load_col_inputs(ColIn<Lay>& ci, int tid, int lane, int wp, int p0,
-                                                int M, const SampleArgs& sa,
+__device__ __forceinline__ void load_col_inputs(ColIn<Lay>& ci, int tid, int lane, int wp,
+                                                const PosMap& pos, int M, const SampleArgs& sa,
                                                 const TargetArgs& ta) {
   if (kMode == kGreedy) return;
   const int32_t* src = kMode == kTarget ? ta.token : sa.row;
 #pragma unroll
   for (int j = 0; j < Lay::kNJ; ++j) {
-    const int p = p0 + wp * 64 + Lay::col(j, lane);
+    const int p = pos(wp * 64 + Lay::col(j, lane));
     ci.col[j] = p < M ? src[p] : -1;
   }
 }
@@ -284,7 +303,7 @@ __device__ __forceinline__ void column_stats(typename Lay::Arr& acc, int j, int 
 template <class Lay, int kMode, bool kFull>
 __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned char* smem,
                                               int tid, int lane, int wv, int wp, int vt, int v0,
-                                              int p0, int M, int V,
+                                              const PosMap& pos, int M, int V,
                                               float4* __restrict__ partials, const SampleArgs& sa,
                                               const TargetArgs& ta, const ColIn<Lay>& ci) {
   constexpr bool kDraw = kMode == kDrawn;
@@ -293,8 +312,9 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
   float4* sred = red + 2 * kTileP;                // [2][kTileP], drawn candidates
   const int vbase = v0 + wv * 128;
   const bool leader = lane < Lay::kLeaders;
-  // the draw's row of position p0 + tid, for the store after the exchange
-  const int own_row = (kDraw && tid < kTileP && p0 + tid < M) ? sa.row[p0 + tid] : -1;
+  // the draw's row of this thread's position, for the store after the exchange
+  const int own_pos = pos(tid < kTileP ? tid : 0);
+  const int own_row = (kDraw && tid < kTileP && own_pos < M) ? sa.row[own_pos] : -1;
 #pragma unroll
   for (int j = 0; j < Lay::kNJ; ++j) {
     float m, s, t;
@@ -315,7 +335,7 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
               zt = Lay::get(acc, i, j, e);
               hit = true;
             }
-        if (hit) ta.z[p0 + col] = zt;
+        if (hit) ta.z[pos(col)] = zt;
       }
     }
     if (kDraw) {
@@ -364,7 +384,7 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
   }
   __syncthreads();
   if (tid < kTileP) {
-    const int r = p0 + tid;
+    const int r = own_pos;
     if (r < M) {
       partials[(size_t)vt * M + r] = merge2(red[tid], red[kTileP + tid]);
       if (kDraw && own_row >= 0) {
@@ -379,15 +399,15 @@ __device__ __forceinline__ void epilogue_tile(typename Lay::Arr& acc, unsigned c
 
 template <class Lay, int kMode>
 __device__ __forceinline__ void epilogue(typename Lay::Arr& acc, unsigned char* smem, int tid,
-                                         int lane, int wv, int wp, int vt, int v0, int p0, int M,
+                                         int lane, int wv, int wp, int vt, int v0, const PosMap& pos, int M,
                                          int V, float4* __restrict__ partials,
                                          const SampleArgs& sa, const TargetArgs& ta,
                                          const ColIn<Lay>& ci) {
   if (v0 + kTileV <= V)
-    epilogue_tile<Lay, kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa,
+    epilogue_tile<Lay, kMode, true>(acc, smem, tid, lane, wv, wp, vt, v0, pos, M, V, partials, sa,
                                     ta, ci);
   else
-    epilogue_tile<Lay, kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials,
+    epilogue_tile<Lay, kMode, false>(acc, smem, tid, lane, wv, wp, vt, v0, pos, M, V, partials,
                                      sa, ta, ci);
 }
 
@@ -407,7 +427,7 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-template <int kMode>
+template <int kMode, bool kIlv = false>
 __device__ __forceinline__ void gemm_stats_bf16_body(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ W, int M, int d,
     int V, int nvt, int npt, float4* __restrict__ partials, const int32_t* __restrict__ rowlist,
@@ -425,6 +445,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   map_tile(blockIdx.x, nvt, npt, vt, pt);
   const int v0 = vt * kTileV;
   const int p0 = pt * kTileP;
+  const PosMap pos{p0, pt, npt, kIlv};
 
   const int row_bytes = d * 2;
   const int kchunks = row_bytes >> 4;      // 16-byte chunks per row
@@ -435,13 +456,14 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   const unsigned recW = (unsigned)(min(kTileV, V - v0) * row_bytes);
   // With a row list, position p of the tile is hidden row rowlist[p0 + p]
   // (outside [0, Mh): no row, reads as zero) and the descriptor spans all Mh
-  // rows.
-  const unsigned recH = rowlist ? (unsigned)(Mh * row_bytes)
-                                : (unsigned)(min(kTileP, M - p0) * row_bytes);
+  // rows; interleaved positions (kIlv) span all M rows too.
+  const bool whole = rowlist != nullptr || kIlv;
+  const unsigned recH = whole ? (unsigned)((rowlist ? Mh : M) * row_bytes)
+                              : (unsigned)(min(kTileP, M - p0) * row_bytes);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(W + (size_t)v0 * row_bytes), (short)0, (int)recW, kBufferWord3);
   const __amdgpu_buffer_rsrc_t rsH = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(hidden + (rowlist ? (size_t)0 : (size_t)p0 * row_bytes)), (short)0, (int)recH,
+      (void*)(hidden + (whole ? (size_t)0 : (size_t)p0 * row_bytes)), (short)0, (int)recH,
       kBufferWord3);
 
   // Each load instruction of a wave writes 1 KiB of LDS = 8 rows x 128 B;
@@ -460,6 +482,9 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   for (int q = 0; q < 4; ++q) {
     qoff[q] = ((q & 1) ? off1 : off0) + (unsigned)q * qstride;
     hoff[q] = qoff[q];
+    if (kIlv)
+      hoff[q] = (unsigned)(pos(drow + 8 * q) * row_bytes) +
+                (unsigned)(((q & 1) ? dchunk1 : dchunk0) << 4);
     if (rowlist) {
       const int p = p0 + drow + 8 * q;
       const int r = p < M ? rowlist[p] : -1;
@@ -621,7 +646,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     ws2 = ws2 == 2 ? 0 : ws2 + 1;
   }
   ColIn<Acc16> ci;
-  load_col_inputs<Acc16, kMode>(ci, tid, lane, wp, p0, M, sa, ta);
+  load_col_inputs<Acc16, kMode>(ci, tid, lane, wp, pos, M, sa, ta);
   step(NoSync{}, a, b0, b1, ws, hs, 1, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -631,7 +656,7 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
-  epilogue<Acc16, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta, ci);
+  epilogue<Acc16, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, pos, M, V, partials, sa, ta, ci);
 }
 
 // fp32 inputs: register-staged double buffer, two v_mfma_f32_32x32x2f32 per
@@ -737,8 +762,9 @@ __device__ __forceinline__ void gemm_stats_f32_body(
   }
 
   ColIn<Acc32> ci;
-  load_col_inputs<Acc32, kMode>(ci, tid, lane, wp, p0, M, sa, ta);
-  epilogue<Acc32, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, p0, M, V, partials, sa, ta, ci);
+  const PosMap pos{p0, pt, npt, false};
+  load_col_inputs<Acc32, kMode>(ci, tid, lane, wp, pos, M, sa, ta);
+  epilogue<Acc32, kMode>(acc, smem, tid, lane, wv, wp, vt, v0, pos, M, V, partials, sa, ta, ci);
 }
 
 // Entry points: positions = hidden rows 0..M-1, or gathered through a row
@@ -780,6 +806,12 @@ __device__ __forceinline__ void gemm_stats_f32_body(
   }
 FORK_GEMM_ENTRIES(bf16)
 FORK_GEMM_ENTRIES(f32)
+// Drawing over all rows with interleaved positions (M = 256 * npt).
+__global__ __launch_bounds__(kThreads) void gemm_stats_bf16_draw_ilv_kernel(FORK_GEMM_ARGS,
+                                                                           SampleArgs sa) {
+  gemm_stats_bf16_body<kDrawn, true>(hidden, W, M, d, V, nvt, npt, partials, nullptr, M, sa,
+                                     TargetArgs{});
+}
 #undef FORK_GEMM_ARGS
 #undef FORK_GEMM_ENTRIES
 
@@ -808,6 +840,8 @@ hipError_t launch_gemm_stats(const void* hidden, const void* W, bool bf16, int M
     FORK_LAUNCH(gemm_stats_f32_target_kernel, target);
   else if (bf16 && rowlist && draw)
     FORK_LAUNCH(gemm_stats_bf16_rows_draw_kernel, rowlist, Mh, sample);
+  else if (bf16 && draw && npt > 1 && M == npt * kTileP && (long long)M * d * 2 < (1LL << 31))
+    FORK_LAUNCH(gemm_stats_bf16_draw_ilv_kernel, sample);
   else if (bf16 && rowlist)
     FORK_LAUNCH(gemm_stats_bf16_rows_kernel, rowlist, Mh);
   else if (bf16 && draw)

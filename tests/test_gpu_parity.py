@@ -443,6 +443,50 @@ def test_drawn_candidates_ragged_and_mode_invariant(B, L, d, V, dtype, BL):
     record(rep, "ragged", shape=[B, L, d, V, BL], temperature=temperature)
 
 
+@pytest.mark.parametrize("B,L,d,V,BL", [(4, 256, 1024, 32000, 32), (2, 384, 264, 1013, 16),
+                                         (8, 512, 4096, 126464, 32)])
+def test_drawn_all_rows_interleaved_positions(B, L, d, V, BL):
+    """Drawing over all rows when B*L is a multiple of 256 (more than one
+    position tile) runs the LM-head kernel whose position tiles take
+    interleaved 16-row chunks.  Rows whose candidates are not drawn equal
+    the greedy step bit for bit; drawn rows equal the active-rows mode bit
+    for bit and the oracle's draws."""
+    _need_gpu()
+    M = B * L
+    assert M % 256 == 0 and M // 256 > 1
+    gen = torch.Generator().manual_seed(5 * B + L + d + V)
+    h = (torch.randn(M, d, generator=gen) * 2.0).to(torch.bfloat16)
+    W = (torch.randn(V, d, generator=gen) / math.sqrt(d)).to(torch.bfloat16)
+    rng = np.random.default_rng(M + V + 7)
+    msk = (rng.random(M) < 0.6).astype(np.uint8)
+    tok = np.where(msk, -1, rng.integers(0, V, M)).astype(np.int32)
+    bs = (rng.integers(0, L // BL, B) * BL).astype(np.int32)
+    hd, Wd = h.to(DEV), W.to(DEV)
+    active = _active_rows(types.SimpleNamespace(B=B, L=L, block_len=BL), msk, bs)
+    other = np.setdiff1d(np.arange(M), active)
+    temperature, counter = 0.8, 77
+    a = gpu_step(hd, Wd, tok, msk, bs, B, L, BL, 0.9, temperature=temperature, seed=SEED,
+                 counter=counter)
+    g = gpu_step(hd, Wd, tok, msk, bs, B, L, BL, 0.9)
+    b = gpu_step(hd, Wd, tok, msk, bs, B, L, BL, 0.9, temperature=temperature, seed=SEED,
+                 counter=counter, rows_mode=_binding.FORK_ROWS_ACTIVE)
+    for k in ("conf", "entropy", "logp", "lse"):
+        x, y = getattr(a, k)[other], getattr(g, k)[other]
+        assert np.array_equal(x.view(np.int32), y.view(np.int32)), k
+    assert np.array_equal(a.argmax[other], g.argmax[other])
+    _same_on_active(a, b, active)
+    hb, Wb = host_bits(h), host_bits(W)
+    rows = active[:: max(1, active.size // 64)] if active.size else active
+    rep = Report()
+    if rows.size:
+        st = oracle.row_stats(hb, Wb, rows)
+        sm = oracle.row_sample(hb, Wb, rows, temperature, SEED, counter)
+        compare_sampled(a, st, sm, rows, hb, Wb, d, temperature, SEED, counter, rep)
+    _say("interleaved drawn %s: %d active rows, %d checked (%d near-tie)" % (
+        (B, L, d, V, BL), active.size, rep.rows, rep.near_tie_rows))
+    record(rep, "interleaved_drawn", shape=[B, L, d, V, BL], temperature=temperature)
+
+
 def test_drawn_candidates_change_with_counter_and_seed():
     """Different counters or seeds give different draws; the same ones give
     the same bits."""
