@@ -46,10 +46,12 @@ def _rm(x, B, L):
 
 
 def _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule,
-         layout=_binding.FORK_LAYOUT_ROW_MAJOR):
+         layout=_binding.FORK_LAYOUT_ROW_MAJOR, outputs="all"):
     """fork_select on row-major host state; with the position-major layout
     the per-position arrays are transposed for the call and back after it,
-    so the results compare directly."""
+    so the results compare directly.  outputs: "all" asks for the commit
+    counts and positions, "ncommit" for the counts only, "none" for
+    neither (their slots then come back as -9)."""
     t = lambda x: torch.as_tensor(np.ascontiguousarray(x), device=DEV)
     pm = layout == _binding.FORK_LAYOUT_POSITION_MAJOR
     lay = (lambda x: _pm(x, B, L)) if pm else (lambda x: x)
@@ -58,8 +60,9 @@ def _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule,
     nc = torch.full((B,), -9, dtype=torch.int32, device=DEV)
     cp = torch.full((B * BL,), -9, dtype=torch.int32, device=DEV)
     _binding.select(t(lay(conf)), t(lay(am)), tok_d, msk_d, bs_d, BL, tau, fb, B=B, L=L,
-                    rule=rule, entropy=t(lay(ent)), uniform=t(uni), out_ncommit=nc,
-                    out_commit_pos=cp, layout=layout)
+                    rule=rule, entropy=t(lay(ent)), uniform=t(uni),
+                    out_ncommit=nc if outputs in ("all", "ncommit") else None,
+                    out_commit_pos=cp if outputs == "all" else None, layout=layout)
     torch.cuda.synchronize()
     back = (lambda x: _rm(x, B, L)) if pm else (lambda x: x)
     return (back(tok_d.cpu().numpy()), back(msk_d.cpu().numpy()), bs_d.cpu().numpy(),
@@ -147,7 +150,8 @@ def test_bad_block_start_reported_in_data_on_both_paths(B):
 
 
 @pytest.mark.parametrize("B", [1 << 16, 1 << 18])
-def test_position_major_sweep_shape_matches_row_major(B):
+@pytest.mark.parametrize("outputs", ["all", "none"])
+def test_position_major_sweep_shape_matches_row_major(B, outputs):
     """The benchmark's sweep shape (blocks of 32 positions, one block per
     sequence, every sequence falling back), 2^16 sequences (one per lane)
     and 2^18 (four per lane): position-major and row-major give the same
@@ -163,28 +167,41 @@ def test_position_major_sweep_shape_matches_row_major(B):
     bs = np.zeros(B, np.int32)
     ent = np.zeros(B * L, np.float32)
     uni = np.zeros(B, np.float32)
-    a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.9, 0)
+    a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.9, 0, outputs=outputs)
     b = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, 0.9, 0,
-             _binding.FORK_LAYOUT_POSITION_MAJOR)
+             _binding.FORK_LAYOUT_POSITION_MAJOR, outputs=outputs)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
-    assert np.all(a[3] == 1) and np.all(a[5][:, 0] == 5) and np.all(a[5][:, 1:] == -1)
+    assert np.all(a[3] == 1)
+    if outputs == "all":
+        assert np.all(a[5][:, 0] == 5) and np.all(a[5][:, 1:] == -1)
     assert np.array_equal(a[0].reshape(B, L)[:, 5], am.reshape(B, L)[:, 5])
+    assert np.all(a[1].reshape(B, L)[:, :6] == 0) and np.all(a[1].reshape(B, L)[:, 6:] == 1)
 
 
 @pytest.mark.parametrize("B,L,BL", [((1 << 18), 40, 32), ((1 << 18) + 2, 33, 16),
                                     ((1 << 18), 20, 20)])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4])
-def test_position_major_large_batches_match_row_major(B, L, BL, rule):
+@pytest.mark.parametrize("outputs", ["all", "ncommit", "none"])
+def test_position_major_large_batches_match_row_major(B, L, BL, rule, outputs):
     """Batches large enough for four sequences per lane (and one not a
     multiple of four): random states, half of them sharing a block start,
-    position-major against row-major (itself checked against the oracle)."""
+    position-major against row-major (itself checked against the oracle).
+    Without the commit positions, groups of four sequences that commit one
+    position each, the same one, take the vector commit."""
     _need_gpu()
     conf, ent, am, tok, msk, bs, uni = _state(B, L, 1000, B + L + BL + rule)
     bs[: B // 2] = min(L - BL, 2)
+    # a quarter of the sequences: one masked position, the same in each group
+    # of four, so the vector commit runs for every rule
+    q = B // 4
+    msk.reshape(B, L)[:q] = 0
+    msk.reshape(B, L)[:q, min(L - BL, 2) + 1] = 1
     for tau in (0.3, 0.9):
-        a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule)
+        a = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule, outputs=outputs)
         b = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule,
-                 _binding.FORK_LAYOUT_POSITION_MAJOR)
+                 _binding.FORK_LAYOUT_POSITION_MAJOR, outputs=outputs)
         for k, (x, y) in enumerate(zip(a, b)):
             assert np.array_equal(x, y), k
+        if outputs != "all":
+            assert np.all(a[5] == -9) and (outputs == "ncommit" or np.all(a[4] == -9))
