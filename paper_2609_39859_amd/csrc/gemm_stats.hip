@@ -556,8 +556,13 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   // kSync >= 0: the stage barrier (with its wait for the next stage's data)
   // comes after the MFMAs of rows 0..kSync, so that queued MFMAs cover it;
   // every read of the step follows the barrier.
-  auto step = [&](auto sync_tag, bf16x8 (&a)[8], const bf16x8 (&bc)[4], bf16x8 (&bn)[4],
-                  int wsn, int hsn, int kkn, int dma, int s_dma, int slot_dma) {
+  // kLive: the wave's 64 positions include one below M.  A wave whose
+  // positions all lie past M (a last position tile with fewer than 256
+  // positions) issues no MFMAs and reads no fragments; it still loads its
+  // share of every stage and takes every barrier.
+  auto step = [&](auto live_tag, auto sync_tag, bf16x8 (&a)[8], const bf16x8 (&bc)[4],
+                  bf16x8 (&bn)[4], int wsn, int hsn, int kkn, int dma, int s_dma, int slot_dma) {
+    constexpr bool kLive = decltype(live_tag)::value;
     constexpr int kSync = decltype(sync_tag)::value;
     // Reads held back by the barrier (kSync >= 0), in this order: a[0..kSync],
     // then bn[0..3]; row kSync + 1 + r takes item r after its second MFMA
@@ -571,17 +576,19 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
     };
     auto row = [&](int i) {
       const int r = i - kSync - 1;
-      acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[0], acc[i][0], 0, 0, 0);
-      acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[1], acc[i][1], 0, 0, 0);
-      if (kSync < 0) {
-        if (i < 4) bn[i] = rd_b(hsn, kkn, i);
-      } else if (r >= 0 && r < kItems) {
-        held(r);
+      if (kLive) {
+        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[0], acc[i][0], 0, 0, 0);
+        acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[1], acc[i][1], 0, 0, 0);
+        if (kSync < 0) {
+          if (i < 4) bn[i] = rd_b(hsn, kkn, i);
+        } else if (r >= 0 && r < kItems) {
+          held(r);
+        }
+        acc[i][2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[2], acc[i][2], 0, 0, 0);
+        acc[i][3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[3], acc[i][3], 0, 0, 0);
+        if (kSync < 0 || r >= 0) a[i] = rd_a(wsn, kkn, i);
+        if (kSync >= 0 && r >= 0 && r < kExtra) held(kRows + r);
       }
-      acc[i][2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[2], acc[i][2], 0, 0, 0);
-      acc[i][3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bc[3], acc[i][3], 0, 0, 0);
-      if (kSync < 0 || r >= 0) a[i] = rd_a(wsn, kkn, i);
-      if (kSync >= 0 && r >= 0 && r < kExtra) held(kRows + r);
       if (dma == 1 && i < 4) issue_W1(s_dma, slot_dma, i);
       if (dma == 2 && i >= 2 && i < 6) issue_H1(s_dma, slot_dma, i - 2);
     };
@@ -601,7 +608,8 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
 #pragma unroll
       for (int i = 0; i <= kSync; ++i) row(i);
 #pragma unroll
-      for (int i = 0; i <= kSync; ++i) order(i);
+      for (int i = 0; i <= kSync; ++i)
+        if (kLive) order(i);
       __builtin_amdgcn_sched_barrier(0);
       // the next stage's hidden and W resident; all reads of this stage returned
       wait_vm_lgkm0<4>();
@@ -611,11 +619,15 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
 #pragma unroll
     for (int i = kSync + 1; i < 8; ++i) row(i);
 #pragma unroll
-    for (int i = kSync + 1; i < 8; ++i) order(i);
+    for (int i = kSync + 1; i < 8; ++i)
+      if (kLive) order(i);
   };
   using NoSync = std::integral_constant<int, -1>;
   using SyncAfterRow1 = std::integral_constant<int, 1>;
 
+  ColIn<Acc16> ci;
+  auto mainloop = [&](auto live_tag) {
+  constexpr bool kLive = decltype(live_tag)::value;
   bf16x8 a[8], b0[4], b1[4];
   // Load order: H0 W0 W1 H1, then per stage k: W(k+2) during the stage's
   // first K step, H(k+2) during its second, after the stage's barrier (which
@@ -630,29 +642,37 @@ __device__ __forceinline__ void gemm_stats_bf16_body(
   issue_H(1, 1);
   wait_vm_lgkm0<8>();  // H0 and W0 resident
   barrier_nofence();
+  if (kLive) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) a[i] = rd_a(0, 0, i);
+    for (int i = 0; i < 8; ++i) a[i] = rd_a(0, 0, i);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) b0[j] = rd_b(0, 0, j);
+    for (int j = 0; j < 4; ++j) b0[j] = rd_b(0, 0, j);
+  }
   int ws = 0, hs = 0, ws2 = 2;  // W slots of stages k and k + 2, hidden slot of k
   for (int k = 0; k + 1 < nk; ++k) {
     const int ws1 = ws == 2 ? 0 : ws + 1, hs1 = hs ^ 1;
-    step(NoSync{}, a, b0, b1, ws, hs, 1, 1, k + 2, ws2);
+    step(live_tag, NoSync{}, a, b0, b1, ws, hs, 1, 1, k + 2, ws2);
     __builtin_amdgcn_sched_barrier(0);
-    step(SyncAfterRow1{}, a, b1, b0, ws1, hs1, 0, 2, k + 2, hs);
+    step(live_tag, SyncAfterRow1{}, a, b1, b0, ws1, hs1, 0, 2, k + 2, hs);
     __builtin_amdgcn_sched_barrier(0);
     ws = ws1;
     hs = hs1;
     ws2 = ws2 == 2 ? 0 : ws2 + 1;
   }
-  ColIn<Acc16> ci;
   load_col_inputs<Acc16, kMode>(ci, tid, lane, wp, pos, M, sa, ta);
-  step(NoSync{}, a, b0, b1, ws, hs, 1, 0, 0, 0);
+  step(live_tag, NoSync{}, a, b0, b1, ws, hs, 1, 0, 0, 0);
+  if (kLive) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b1[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b1[j], acc[i][j], 0, 0, 0);
+  }
+  };
+  if (pos(wp * 64) < M)
+    mainloop(std::true_type{});
+  else
+    mainloop(std::false_type{});
   __builtin_amdgcn_s_waitcnt(0);
   barrier_nofence();
 
