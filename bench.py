@@ -569,13 +569,13 @@ class StepBench:
         return ms[-1]
 
 
-def config_leg(name, args, dev, hip):
+def config_leg(name, args, dev, hip, cfg=None):
     """Eager and graph-replayed step times of one workload, all rows and
     active-block rows, with the LM head's fraction of the bf16 MFMA peak."""
     import torch
 
     from paper_2609_39859_amd import _binding, synth
-    cfg = synth.CONFIGS[name]
+    cfg = cfg or synth.CONFIGS[name]
     print("bench: workload %s B=%d L=%d d=%d V=%d" % (name, cfg.B, cfg.L, cfg.d, cfg.V),
           file=sys.stderr, flush=True)
     sb = StepBench(cfg, dev, hip)
@@ -776,6 +776,14 @@ def main():
         out["configs"] = {}
         for name in ("mid", "rollout", "long"):
             out["configs"][name] = config_leg(name, args, dev, hip)
+        # One GPU's share of a vocabulary-sharded step over 8 GPUs: the
+        # LLaDA-8B shape with V / 8 rows of W_head (the per-position partials
+        # would then be all-gathered and merged on every GPU; that exchange
+        # is not part of this single-GPU measurement).
+        shard = synth.CONFIGS["llada8b"].with_(name="llada8b_vocab_shard_of_8", V=V // 8)
+        leg = config_leg(shard.name, args, dev, hip, cfg=shard)
+        leg["shards"] = 8
+        out["configs"][shard.name] = leg
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline (~%.0f s)" % args.cpu_seconds, file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, W, hs[0], args.cpu_seconds)
