@@ -120,6 +120,38 @@ def _check_against_oracle(B, L, BL, rule, layout, shared_start=False):
             assert np.all(g[5][b, done.size:] == -1)
 
 
+@pytest.mark.parametrize("B,L,BL", [(4096, 32, 32), (4096, 64, 16), (8192, 48, 8),
+                                    (4160, 64, 32)])
+@pytest.mark.parametrize("rule", [0, 4, 1])
+@pytest.mark.parametrize("outputs", ["all", "none"])
+def test_row_major_whole_wave_blocks(B, L, BL, rule, outputs):
+    """Row-major batches whose blocks start on multiples of 16 positions
+    with 32 positions left in the row (the lane path's wide loads), every
+    other wave with one sequence off that grid (its position-by-position
+    path) and the last sequence idle, under the threshold, leftmost, random
+    and highest-confidence rules, with and without the commit outputs.
+    Against the oracle, bit for bit."""
+    _need_gpu()
+    conf, ent, am, tok, msk, bs, uni = _state(B, L, 1000, B + 7 * L + BL + rule)
+    rng = np.random.default_rng(B + L + BL)
+    bs[:] = rng.choice(np.arange(0, L - 32 + 1, 16), B)
+    for w in range(1, B // 64, 2):
+        bs[64 * w + 5] = min(bs[64 * w + 5] + 1, L)
+    for tau in (0.3, 0.9):
+        g = _run(conf, ent, am, tok, msk, bs, uni, B, L, BL, tau, rule, outputs=outputs)
+        o = oracle.select_ex(conf, am, tok, msk, bs, B, L, BL, float(np.float32(tau)), rule,
+                             entropy=ent, uniform=uni)
+        n = 5 if outputs == "all" else 4
+        for k, (x, y) in enumerate(zip(g[:n], o[:n])):
+            assert np.array_equal(x, y), ("tokens", "mask", "block_start", "fallback", "ncommit")[k]
+        if outputs == "all":
+            for b in range(0, B, 97):
+                sl = slice(b * L, (b + 1) * L)
+                done = np.nonzero(msk[sl] & ~o[1][sl])[0]
+                assert np.array_equal(g[5][b, :done.size], done)
+                assert np.all(g[5][b, done.size:] == -1)
+
+
 def test_lane_and_wave_paths_agree():
     """The first sequences of a large batch (lane path) and the same
     sequences run as a small batch (wave path) give identical results."""
