@@ -16,7 +16,9 @@ the same workload and scales it to steps per second.  `active_rows_mode`
 times the same decode with the LM head restricted to each sequence's active
 block (FORK_ROWS_ACTIVE), a separate, HBM-bound workload; `drawn_candidates`
 times both modes with candidates drawn at sampling temperature 0.8;
-`forkgrpo_likelihood` times one ForkGRPO batch of 4096 teacher-forced
+`decode_loop` times whole decodes from the initial state until no position
+is masked (NFE steps, committed tokens per second), on all rows and on the
+active blocks' rows; `forkgrpo_likelihood` times one ForkGRPO batch of 4096 teacher-forced
 log-probabilities plus its objective; `selection` gives the unmasking
 rule's latency at the real shapes and its HBM bandwidth on a sweep of large
 batches; `measured_peaks` gives this GPU's achievable MFMA and HBM rates
@@ -531,6 +533,42 @@ class StepBench:
             hip.hipEventDestroy(e)
         return start.elapsed_time(stop), lm, wall
 
+    def full_decode(self, rows_mode):
+        """A whole decode from the initial state: steps until no position is
+        masked.  An untimed pass counts the steps (NFE) and fallback steps,
+        checking the mask after every step; the same NFE steps are then
+        timed from the initial state, with no host check inside the timed
+        region, and must end with every position unmasked.  Hidden states
+        cycle through the preloaded batches."""
+        import torch
+        c = self.cfg
+        self.reset()
+        to_commit = int((self.msk != 0).sum())
+        nfe = fallback = parallel = 0
+        while bool((self.msk != 0).any()):
+            self.step(nfe, rows_mode=rows_mode)
+            fb = self.fb.cpu()
+            fallback += int((fb == 1).sum())
+            parallel += int((fb == 0).sum())
+            nfe += 1
+            # every step commits at least one position of each active sequence
+            assert nfe <= to_commit, "decode did not finish"
+        self.reset()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record()
+        for i in range(nfe):
+            self.step(i, rows_mode=rows_mode)
+        stop.record()
+        torch.cuda.synchronize()
+        assert not bool((self.msk != 0).any())
+        ms = start.elapsed_time(stop)
+        self.reset()
+        return {"nfe": nfe, "committed_tokens": to_commit, "ms": ms,
+                "tokens_per_s": to_commit / (ms * 1e-3), "steps_per_s": nfe / (ms * 1e-3),
+                "fallback_seq_steps": fallback, "parallel_seq_steps": parallel,
+                "tokens_per_step": to_commit / nfe / c.B}
+
     def graph_timed(self, steps, rows_mode=0):
         """The same `steps` steps captured into one HIP graph (caller
         workspace) and replayed: the GPU's time per step without host
@@ -586,6 +624,10 @@ def config_leg(name, args, dev, hip, cfg=None):
     g_ms = sb.graph_timed(args.steps)
     a_total, a_lm, _ = sb.timed(_binding.FORK_ROWS_ACTIVE, args.steps, args.warmup)
     a_g_ms = sb.graph_timed(args.steps, _binding.FORK_ROWS_ACTIVE)
+    dec = {"active_rows": sb.full_decode(_binding.FORK_ROWS_ACTIVE)}
+    if cfg.d * cfg.V <= (1 << 30) // 8:
+        # small heads only: a whole decode on all rows stays within a second
+        dec["all_rows"] = sb.full_decode(_binding.FORK_ROWS_ALL)
     tf = flops / (lm_ms * 1e-3) / 1e12
     out = {"workload": "B=%d, L=%d (prompt %d + gen %d), block_len %d, d=%d, V=%d, %s, tau=%g"
                        % (cfg.B, cfg.L, cfg.P, cfg.G, cfg.block_len, cfg.d, cfg.V, cfg.dtype,
@@ -601,7 +643,8 @@ def config_leg(name, args, dev, hip, cfg=None):
            "step_ms_at_60pct_of_peak": flops / (0.6 * PEAK_BF16_TFLOPS * 1e12) * 1e3,
            "active_rows_mode": {"ms_per_step": a_total / args.steps,
                                 "graph_ms_per_step": a_g_ms,
-                                "lmhead_ms": sum(a_lm) / len(a_lm)}}
+                                "lmhead_ms": sum(a_lm) / len(a_lm)},
+           "decode_loop": dec}
     del sb
     torch.cuda.empty_cache()
     return out
@@ -617,6 +660,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-active-rows", action="store_true",
                     help="skip the extra timing of the active-block-only LM head")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the whole-decode timings (committed tokens per second)")
     ap.add_argument("--no-drawn", action="store_true",
                     help="skip the extra timings with candidates drawn at temperature 0.8")
     ap.add_argument("--no-grpo", action="store_true",
@@ -743,6 +788,12 @@ def main():
             ar = out["active_rows_mode"]["roofline"]
             ar["measured_peak"] = pk["hbm_copy_GB_s"]
             ar["frac_of_measured_peak"] = ar["achieved"] / pk["hbm_copy_GB_s"]
+    if not args.no_decode:
+        print("bench: whole decodes (all rows, then active-block rows)", file=sys.stderr,
+              flush=True)
+        out["decode_loop"] = {"all_rows": sb.full_decode(_binding.FORK_ROWS_ALL),
+                              "active_rows": sb.full_decode(_binding.FORK_ROWS_ACTIVE),
+                              "hidden": "%d preloaded batches used in turn" % len(sb.hs)}
     if not args.no_drawn:
         # Candidates drawn at sampling temperature 0.8 (Gumbel-max over
         # Philox4x32-10 draws for the active blocks' positions).
