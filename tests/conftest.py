@@ -40,13 +40,13 @@ def _parity_summary(records):
 def pytest_sessionfinish(session, exitstatus):
     """Write the parity checks' exclusion counts (near-threshold sequences,
     near-tie rows, largest errors) to a JSON record: the path in
-    FORK_PARITY_RECORD, else gpurun_out/parity_counts.json at the repository
-    root."""
+    FORK_PARITY_RECORD, else test_records/parity_counts.json at the
+    repository root."""
     records = _parity_records()
     if not records:
         return
     import json
-    path = os.environ.get("FORK_PARITY_RECORD") or os.path.join(ROOT, "gpurun_out",
+    path = os.environ.get("FORK_PARITY_RECORD") or os.path.join(ROOT, "test_records",
                                                                  "parity_counts.json")
     os.makedirs(os.path.dirname(path), exist_ok=True)
     with open(path, "w") as f:
