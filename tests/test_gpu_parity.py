@@ -652,11 +652,13 @@ def test_full_size_active_rows_mode(name):
     record(rep, name, steps=1, rows_mode=1, tau=cfg.tau)
 
 
-@pytest.mark.parametrize("name,rows_mode", [("llada8b", 0), ("llada8b", 1), ("rollout", 1)])
+@pytest.mark.parametrize("name,rows_mode", [("llada8b", 0), ("llada8b", 1), ("rollout", 0),
+                                            ("rollout", 1)])
 def test_full_size_drawn_candidates(name, rows_mode):
     """Drawn candidates at the full sizes (temperature 0.8, as in the
-    paper's tuned Fork-dLLM setting): the active rows of the first two
-    sequences against the oracle's draws."""
+    paper's tuned Fork-dLLM setting): the active rows of the first two and
+    the last sequence against the oracle's draws (over all rows, the
+    rollout batch spreads its drawn blocks over 96 position tiles)."""
     _need_gpu()
     cfg = synth.CONFIGS[name]
     W = synth.weights(cfg, device=DEV)
@@ -665,7 +667,8 @@ def test_full_size_drawn_candidates(name, rows_mode):
     _say("full-size drawn %s mode %d: GPU step" % (name, rows_mode))
     g = gpu_step(h, W, tok, msk, bs, cfg.B, cfg.L, cfg.block_len, cfg.tau, rows_mode=rows_mode,
                  temperature=0.8, seed=SEED, counter=2)
-    rows = _active_rows(cfg, msk, bs)[: 2 * cfg.block_len]
+    act = _active_rows(cfg, msk, bs)
+    rows = np.concatenate([act[: 2 * cfg.block_len], act[-cfg.block_len:]])
     hb, Wb = host_bits(h), host_bits(W)
     st = oracle.row_stats(hb, Wb, rows)
     sm = oracle.row_sample(hb, Wb, rows, 0.8, SEED, 2)
