@@ -470,8 +470,8 @@ PAPER_CONTEXT = {
     "sampler_nfe": "Fork-dLLM needs 2-3x fewer model evaluations per sample than AR decoding "
                    "at matched pass@k; LLaDA-8B-Instruct, generation length 256, blocks of 32, "
                    "lambda = tau = 0.8: NFE 67.8 vs 227.9 (GSM8K), 92.3 vs 243.3 (MATH-500), "
-                   "108.4 vs 242.3 (HumanEval), 75.8 vs 192.3 (MBPP) (Section 4, pass@k table "
-                   "for LLaDA-8B-Instruct)",
+                   "108.4 vs 242.3 (HumanEval), 75.8 vs 192.3 (MBPP) (Section 4.1; the appendix's "
+                   "pass@k table for LLaDA-8B-Instruct)",
     "post_training_cost": "ForkGRPO with LoRA on 4 x H100 for 12 h (48 H100-hours) against the "
                           "JustGRPO checkpoint from full fine-tuning on 16 x H100 for 24 h "
                           "(384 H100-hours): 8x fewer H100-hours at comparable GSM8K accuracy "
